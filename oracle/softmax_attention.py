@@ -1,0 +1,148 @@
+"""Plain fp64 CPU oracle for softmax attention (the operator the fused kernel computes).
+
+TEST INFRASTRUCTURE ONLY: used by ``tests/``, ``__graft_entry__.smoke()`` and
+the CPU-baseline leg of ``bench.py``; never by the product path.
+
+What it follows
+---------------
+The paper states the problem in its Background, subsection "Attention
+Operators and acceleration": with Q, K, V holding N tokens of dimension d,
+Attention(Q, K, V) = Softmax(Mask(Q K^T / sqrt(d))) V, evaluated independently
+for every (batch, head).  A FlashAttention-style kernel reaches exactly this
+value (up to rounding order); it only reorders the work.  So this oracle is the
+definition written out, per (batch, head):
+
+1. decode the 16-bit inputs to fp64 exactly (:func:`decode_fp64`);
+2. scores s_ij = scale * (q_i . k_j) in fp64 (:func:`scores_fp64`); the scale
+   is a parameter, taken as the same fp32 value the kernel receives;
+3. mask: with ``causal``, key j is visible to query i iff j <= i; a masked
+   score is -inf (the paper leaves "Mask" undefined; the Evaluation section
+   only names "causal masks");
+4. row softmax with the row maximum subtracted (the paper's Appendix B
+   listing computes the softmax "with Smax and Ssum"), giving P and the
+   natural-log log-sum-exp lse_i = m_i + ln(sum_j exp(s_ij - m_i))
+   (:func:`softmax_rows_fp64`);
+5. O = P V (:func:`attention_fp64`).
+
+Queries are processed in independent row blocks only to bound memory; each
+row's value is the definition's.  There is no online rescaling, no key
+blocking and no fusion.
+
+Readings where the paper is silent: the head layout is [B, H, N, d]; lse is
+the natural logarithm; the scale is applied to the exact dot product, never to
+16-bit Q.
+
+Pins: ``tests/test_oracle.py`` checks every function here against a
+high-precision brute force, closed forms, invariants and special cases, and
+shows that planted mistakes fail those pins.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+_F64_DTYPES = ("f16", "bf16", "f64")
+
+
+def decode_fp64(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Decode stored inputs to fp64, exactly.
+
+    ``f16``: ``numpy.float16`` values; ``bf16``: ``uint16`` bit patterns (the
+    top half of an IEEE fp32); ``f64``: already fp64 (used by the pins).
+    """
+    if dtype == "f16":
+        if x.dtype != np.float16:
+            raise TypeError("f16 input must be numpy.float16")
+        return x.astype(np.float64)
+    if dtype == "bf16":
+        if x.dtype != np.uint16:
+            raise TypeError("bf16 input must be uint16 bit patterns")
+        return (x.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+    if dtype == "f64":
+        return np.asarray(x, dtype=np.float64)
+    raise ValueError(f"unknown dtype {dtype!r}; expected one of {_F64_DTYPES}")
+
+
+def scores_fp64(Q: np.ndarray, K: np.ndarray, scale: float, causal: bool,
+                row0: int = 0) -> np.ndarray:
+    """Masked scaled scores for one (batch, head).
+
+    ``Q``: [R, d] fp64 queries whose global row indices are row0 .. row0+R-1;
+    ``K``: [Nk, d] fp64 keys.  Returns S [R, Nk] with s_ij = scale * (q_i . k_j)
+    and -inf where the causal mask hides key j from query i (j > i).
+    """
+    S = (Q @ K.T) * np.float64(scale)
+    if causal:
+        rows = np.arange(row0, row0 + Q.shape[0])[:, None]
+        cols = np.arange(K.shape[0])[None, :]
+        S = np.where(cols > rows, -np.inf, S)
+    return S
+
+
+def softmax_rows_fp64(S: np.ndarray):
+    """Row softmax of masked scores with the row maximum subtracted.
+
+    Returns (P, lse): P [R, Nk] with rows summing to 1, and the natural-log
+    log-sum-exp lse [R].  Every row must have at least one finite score (a
+    causal square mask always leaves key 0 visible).
+    """
+    m = S.max(axis=1, keepdims=True)
+    E = np.exp(S - m)
+    l = E.sum(axis=1, keepdims=True)
+    P = E / l
+    lse = m[:, 0] + np.log(l[:, 0])
+    return P, lse
+
+
+def attention_fp64(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float,
+                   causal: bool, dtype: str, row_block: int = 256):
+    """Exact attention forward for every (batch, head) of [B, H, N, d] inputs.
+
+    Returns (O [B, H, N, d] fp64, lse [B, H, N] fp64).
+    """
+    B, H, N, d = q.shape
+    if k.shape != (B, H, N, d) or v.shape != (B, H, N, d):
+        raise ValueError("q, k, v must share the shape [B, H, N, d]")
+    scale64 = float(np.float32(scale)) if dtype != "f64" else float(scale)
+    O = np.empty((B, H, N, d), dtype=np.float64)
+    lse = np.empty((B, H, N), dtype=np.float64)
+    for b in range(B):
+        for h in range(H):
+            K = decode_fp64(k[b, h], dtype)
+            V = decode_fp64(v[b, h], dtype)
+            for r0 in range(0, N, row_block):
+                r1 = min(N, r0 + row_block)
+                Q = decode_fp64(q[b, h, r0:r1], dtype)
+                S = scores_fp64(Q, K, scale64, causal, row0=r0)
+                P, lse_blk = softmax_rows_fp64(S)
+                O[b, h, r0:r1] = P @ V
+                lse[b, h, r0:r1] = lse_blk
+    return O, lse
+
+
+def attention_rows_fp64(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float,
+                        causal: bool, dtype: str, rows):
+    """Exact attention output for selected rows only.
+
+    ``rows``: iterable of (b, h, i).  Returns (O [R, d] fp64, lse [R] fp64) in
+    the order given.  Used where the full output is too large for the CPU:
+    each selected row is the definition's value, computed from that row's
+    query against all of its (visible) keys.
+    """
+    rows = [tuple(int(t) for t in r) for r in rows]
+    d = q.shape[-1]
+    O = np.empty((len(rows), d), dtype=np.float64)
+    lse = np.empty(len(rows), dtype=np.float64)
+    scale64 = float(np.float32(scale)) if dtype != "f64" else float(scale)
+    by_head = {}
+    for idx, (b, h, i) in enumerate(rows):
+        by_head.setdefault((b, h), []).append((idx, i))
+    for (b, h), items in by_head.items():
+        K = decode_fp64(k[b, h], dtype)
+        V = decode_fp64(v[b, h], dtype)
+        for idx, i in items:
+            Q = decode_fp64(q[b, h, i:i + 1], dtype)
+            S = scores_fp64(Q, K, scale64, causal, row0=i)
+            P, lse_row = softmax_rows_fp64(S)
+            O[idx] = (P @ V)[0]
+            lse[idx] = lse_row[0]
+    return O, lse

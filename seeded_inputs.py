@@ -1,0 +1,112 @@
+"""Seeded synthetic attention inputs, shared by the oracle side and the HIP side.
+
+This module draws Q, K and V and rounds them to the 16-bit storage type. It
+holds none of the attention arithmetic: the oracle (``oracle/``) and the HIP
+library each decode and compute on their own.
+
+Recipe (the paper benchmarks on unstated, presumably random inputs; these
+stand in for its long-context workloads of the Evaluation section's
+"Benchmark setting"):
+
+* ``rng = numpy.random.default_rng(seed)`` (PCG64), seed 0 unless stated;
+* draw ``standard_normal(shape, float32)`` for Q, then K, then V, each of
+  shape ``[B, H, N, d]``;
+* optionally multiply Q and K by an exact power of two in fp32 (the sharper
+  long-context workload uses 2);
+* round to fp16 (numpy's cast, round-to-nearest-even) or to bf16 with
+  round-to-nearest-even on the fp32 bit pattern.
+
+bf16 arrays are returned as ``uint16`` bit patterns, because numpy has no
+bfloat16 type; fp16 arrays are ``numpy.float16``.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+DTYPES = ("f16", "bf16")
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round fp32 values to bf16 (round-to-nearest-even); return the uint16 bits.
+
+    Finite inputs only (the generator never produces inf or NaN).
+    """
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    lsb = (u >> np.uint32(16)) & np.uint32(1)
+    rounded = u + np.uint32(0x7FFF) + lsb
+    return (rounded >> np.uint32(16)).astype(np.uint16)
+
+
+def round_to_storage(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Round an fp32 array to the 16-bit storage type named by ``dtype``."""
+    if dtype == "f16":
+        return np.ascontiguousarray(x, dtype=np.float32).astype(np.float16)
+    if dtype == "bf16":
+        return f32_to_bf16_bits(x)
+    raise ValueError(f"unknown dtype {dtype!r}; expected one of {DTYPES}")
+
+
+def make_qkv(B: int, H: int, N: int, d: int, dtype: str, seed: int = 0,
+             qk_mult: float = 1.0):
+    """Draw Q, K, V of shape [B, H, N, d] and round them to ``dtype``.
+
+    Returns three contiguous arrays (``float16`` or bf16 ``uint16`` bits).
+    """
+    if dtype not in DTYPES:
+        raise ValueError(f"unknown dtype {dtype!r}")
+    rng = np.random.default_rng(seed)
+    shape = (B, H, N, d)
+    out = []
+    for name in ("q", "k", "v"):
+        x = rng.standard_normal(shape, dtype=np.float32)
+        if name in ("q", "k") and qk_mult != 1.0:
+            x *= np.float32(qk_mult)
+        out.append(round_to_storage(x, dtype))
+        del x
+    return tuple(out)
+
+
+def default_scale(d: int) -> float:
+    """The softmax scale 1/sqrt(d), as the fp32 value handed to the kernel."""
+    return float(np.float32(1.0 / np.sqrt(np.float64(d))))
+
+
+@dataclass(frozen=True)
+class Workload:
+    """One synthetic attention workload: shapes, storage type, masks, input recipe."""
+    name: str
+    B: int
+    H: int
+    N: int
+    d: int
+    dtype: str
+    causal: tuple = field(default=(False,))
+    qk_mult: float = 1.0
+    seed: int = 0
+
+    @property
+    def scale(self) -> float:
+        return default_scale(self.d)
+
+    def inputs(self):
+        return make_qkv(self.B, self.H, self.N, self.d, self.dtype,
+                        seed=self.seed, qk_mult=self.qk_mult)
+
+
+WORKLOADS = {
+    w.name: w for w in (
+        Workload("mha_b1_h2_n128_d64_f16", 1, 2, 128, 64, "f16", (False,)),
+        Workload("mha_b8_h16_n1024_d64_f16", 8, 16, 1024, 64, "f16", (False,)),
+        Workload("mha_b4_h32_n2048_d128_f16_causal", 4, 32, 2048, 128, "f16", (True,)),
+        Workload("mha_b2_h32_n8192_d128_bf16", 2, 32, 8192, 128, "bf16", (False, True)),
+        Workload("mha_b1_h32_n32768_d128_bf16_causal_qk2", 1, 32, 32768, 128, "bf16",
+                 (True,), qk_mult=2.0),
+    )
+}
+
+# The workload the throughput figure is quoted on (N = 8192, d = 128).
+BENCH_WORKLOAD = "mha_b2_h32_n8192_d128_bf16"
+# The small workload that the full oracle finishes in well under a second.
+SMOKE_WORKLOAD = "mha_b1_h2_n128_d64_f16"
