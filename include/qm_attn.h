@@ -1,0 +1,95 @@
+/*
+ * qm_attn.h - fused scaled-dot-product attention forward for AMD MI355X (gfx950).
+ *
+ * The operation is the paper's statement of the attention problem (Background,
+ * subsection "Attention Operators and acceleration"): for queries Q, keys K and
+ * values V holding N tokens of head dimension d,
+ *
+ *     O = softmax(Mask(scale * Q K^T)) V,     lse_i = ln sum_{j visible} exp(scale * q_i . k_j)
+ *
+ * evaluated independently for every (batch, head), the way the paper's kernels
+ * give each thread block a fixed batch and head of Q (Method, "Parameter
+ * Analysis and Reasoning").  The N x N score matrix is never stored: scores are
+ * formed block by block on chip with an online softmax that keeps a running row
+ * maximum and row sum (the paper's Appendix B listings: "Softmax S with Smax and
+ * Ssum" between the two fused GEMMs).
+ *
+ * Conventions shared by every entry point:
+ *   - All tensor pointers are DEVICE pointers owned by the caller.  The library
+ *     never allocates, frees, retains or synchronises them.
+ *   - q, k, v, o are contiguous row-major [B][H][N][d] arrays of the 16-bit type
+ *     named by `dtype`; o has the input type.  lse is a contiguous [B][H][N]
+ *     float32 array.  Base pointers must be 16-byte aligned.
+ *   - The call validates its arguments on the host, then enqueues one kernel on
+ *     `stream` (NULL = the null stream) and returns; results are valid once the
+ *     caller has synchronised that stream.  On any error nothing is enqueued and
+ *     no output is written.
+ *   - Calls are thread-safe; calls on different streams may run concurrently.
+ */
+#ifndef QM_ATTN_H
+#define QM_ATTN_H
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* 16-bit storage types of q, k, v and o. */
+typedef enum {
+  QM_F16 = 0,  /* IEEE binary16 */
+  QM_BF16 = 1  /* bfloat16 (top half of an IEEE binary32) */
+} qm_dtype_t;
+
+/* Status codes returned by qm_attn_fwd. */
+enum {
+  QM_OK = 0,
+  QM_ERR_NULL = -1,        /* q, k, v, o or lse is NULL */
+  QM_ERR_SHAPE = -2,       /* B, H or N < 1, or B*H*N*d does not fit in 62 bits */
+  QM_ERR_HEADDIM = -3,     /* d is not 64 or 128 */
+  QM_ERR_DTYPE = -4,       /* dtype is not QM_F16 or QM_BF16 */
+  QM_ERR_SCALE = -5,       /* scale is infinite or NaN */
+  QM_ERR_ALIAS = -6,       /* o or lse overlaps q, k, v or each other */
+  QM_ERR_CAUSAL = -7,      /* causal is neither 0 nor 1 */
+  QM_ERR_LAUNCH = -8,      /* the HIP runtime rejected the kernel launch */
+  QM_ERR_UNSUPPORTED = -9  /* a pointer is not 16-byte aligned */
+};
+
+/*
+ * qm_attn_fwd - attention forward for B batches x H heads of N tokens.
+ *
+ *   q, k, v  [in]  device, [B][H][N][d] of `dtype`.  May alias one another.
+ *   o        [out] device, [B][H][N][d] of `dtype`: the attention output,
+ *                  rounded to the storage type (round-to-nearest-even).
+ *   lse      [out] device, [B][H][N] float32: natural-log log-sum-exp of the
+ *                  visible scaled scores of each query row.
+ *   B, H, N        batch, heads, tokens (any N >= 1; tails are masked on chip).
+ *   d              head dimension: 64 or 128 (the paper's head dimensions,
+ *                  Evaluation section, "Benchmark setting").
+ *   scale          any finite float multiplying q_i . k_j (usually 1/sqrt(d)).
+ *                  It is applied to the fp32 dot product, never to 16-bit Q.
+ *   causal         0: every key is visible; 1: key j is visible to query i
+ *                  iff j <= i (the paper's causal mask; fully masked key blocks
+ *                  are skipped, not computed).
+ *   stream         HIP stream to enqueue on (NULL = null stream).
+ *   dtype          a qm_dtype_t.
+ *
+ * Arithmetic: 16-bit products with fp32 accumulation on the matrix cores; the
+ * softmax in fp32; probabilities rounded to `dtype` before the second product.
+ * Results are deterministic: the same inputs give byte-identical outputs.
+ *
+ * Returns QM_OK or one of the QM_ERR_* codes above; every check except
+ * QM_ERR_LAUNCH happens before anything is enqueued.
+ */
+int qm_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
+                int B, int H, int N, int d, float scale, int causal,
+                hipStream_t stream, int dtype);
+
+/* qm_attn_strerror - a static, human-readable string for a status code. */
+const char* qm_attn_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QM_ATTN_H */

@@ -1,0 +1,26 @@
+"""MI355X-native fused attention forward: gfx950 HIP kernels behind a C ABI.
+
+``fwd(q, k, v, causal, scale)`` computes softmax(mask(scale * Q K^T)) V and the
+per-row log-sum-exp for [B, H, N, d] fp16/bf16 tensors on one GPU.  The
+operation and its arguments are documented in ``include/qm_attn.h``.
+"""
+from .binding import (  # noqa: F401
+    LIB_PATH,
+    QM_BF16,
+    QM_ERR_ALIAS,
+    QM_ERR_CAUSAL,
+    QM_ERR_DTYPE,
+    QM_ERR_HEADDIM,
+    QM_ERR_LAUNCH,
+    QM_ERR_NULL,
+    QM_ERR_SCALE,
+    QM_ERR_SHAPE,
+    QM_ERR_UNSUPPORTED,
+    QM_F16,
+    QM_OK,
+    QmAttnError,
+    fwd,
+    load_library,
+    qm_attn_fwd,
+    strerror,
+)

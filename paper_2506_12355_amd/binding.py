@@ -1,0 +1,128 @@
+"""ctypes binding of the C-ABI attention library (include/qm_attn.h).
+
+Argument marshalling only: every step of the attention forward runs in the
+gfx950 kernels.  PyTorch supplies device memory and the current HIP stream.
+There is no fallback: if ``libqm_attn.so`` is missing, loading fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG_DIR, "libqm_attn.so")
+
+# qm_dtype_t
+QM_F16 = 0
+QM_BF16 = 1
+
+# status codes
+QM_OK = 0
+QM_ERR_NULL = -1
+QM_ERR_SHAPE = -2
+QM_ERR_HEADDIM = -3
+QM_ERR_DTYPE = -4
+QM_ERR_SCALE = -5
+QM_ERR_ALIAS = -6
+QM_ERR_CAUSAL = -7
+QM_ERR_LAUNCH = -8
+QM_ERR_UNSUPPORTED = -9
+
+_lib = None
+_lock = threading.Lock()
+
+
+class QmAttnError(RuntimeError):
+    """A non-zero status from the C library."""
+
+    def __init__(self, status: int, message: str):
+        super().__init__(f"qm_attn_fwd failed with status {status}: {message}")
+        self.status = status
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load (once) and return the HIP library; raise if it has not been built."""
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(path):
+            raise RuntimeError(
+                f"{path} is missing: the HIP attention library has not been built "
+                "(run `python -m paper_2506_12355_amd.build`)")
+        lib = ctypes.CDLL(path)
+        lib.qm_attn_fwd.argtypes = [
+            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+            ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+            ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+        ]
+        lib.qm_attn_fwd.restype = ctypes.c_int
+        lib.qm_attn_strerror.argtypes = [ctypes.c_int]
+        lib.qm_attn_strerror.restype = ctypes.c_char_p
+        _lib = lib
+        return lib
+
+
+def strerror(status: int) -> str:
+    return load_library().qm_attn_strerror(int(status)).decode()
+
+
+def qm_attn_fwd(q, k, v, o, lse, B, H, N, d, scale, causal, stream, dtype) -> int:
+    """The C entry point with plain integers for pointers; returns the status."""
+    return load_library().qm_attn_fwd(q, k, v, o, lse, int(B), int(H), int(N), int(d),
+                                      float(scale), int(causal), stream, int(dtype))
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float16:
+        return QM_F16
+    if t.dtype == torch.bfloat16:
+        return QM_BF16
+    raise TypeError(f"q, k, v must be float16 or bfloat16, not {t.dtype}")
+
+
+def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse=None,
+        stream=None):
+    """Attention forward on torch tensors of shape [B, H, N, d] on a ROCm device.
+
+    Returns (o, lse): o has q's shape and dtype, lse is float32 [B, H, N].
+    ``scale`` defaults to 1/sqrt(d) rounded to float32.  ``stream`` defaults
+    to the current stream of q's device.
+    """
+    import torch
+
+    if q.dim() != 4:
+        raise ValueError("q must have shape [B, H, N, d]")
+    if k.shape != q.shape or v.shape != q.shape:
+        raise ValueError("q, k and v must have the same shape")
+    if not (q.is_cuda and k.is_cuda and v.is_cuda):
+        raise ValueError("q, k and v must be on a ROCm device")
+    if not (q.device == k.device == v.device):
+        raise ValueError("q, k and v must be on the same device")
+    if not (q.dtype == k.dtype == v.dtype):
+        raise TypeError("q, k and v must have the same dtype")
+    if not (q.is_contiguous() and k.is_contiguous() and v.is_contiguous()):
+        raise ValueError("q, k and v must be contiguous [B, H, N, d]")
+    B, H, N, d = q.shape
+    code = _dtype_code(q)
+    if scale is None:
+        scale = float(torch.tensor(1.0 / d ** 0.5, dtype=torch.float32))
+    if out is None:
+        out = torch.empty_like(q)
+    elif out.shape != q.shape or out.dtype != q.dtype or not out.is_contiguous():
+        raise ValueError("out must be a contiguous tensor like q")
+    if lse is None:
+        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    elif lse.shape != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous():
+        raise ValueError("lse must be a contiguous float32 tensor of shape [B, H, N]")
+    if stream is None:
+        stream = torch.cuda.current_stream(q.device)
+    with torch.cuda.device(q.device):
+        status = qm_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                             lse.data_ptr(), B, H, N, d, scale, 1 if causal else 0,
+                             stream.cuda_stream, code)
+    if status != QM_OK:
+        raise QmAttnError(status, strerror(status))
+    return out, lse

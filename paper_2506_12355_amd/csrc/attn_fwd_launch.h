@@ -1,0 +1,36 @@
+// Internal interface between the C-ABI front end (qm_attn.cpp) and the gfx950
+// kernels (attn_fwd_gfx950.hip).  Not installed; callers use include/qm_attn.h.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace qm {
+
+// How the kernel conditions Q when it loads it into registers.  Both changes
+// are exact in 16-bit arithmetic, so the kernel can always use a positive
+// exponent-domain scale:
+//   kQNormal  - use Q as stored (scale > 0);
+//   kQNegate  - flip every sign bit (scale < 0: scale*q.k = |scale|*(-q).k);
+//   kQZero    - replace Q by zeros (scale == 0 or too small to change any
+//               score: every visible score is then exactly 0).
+enum QMode : int { kQNormal = 0, kQNegate = 1, kQZero = 2 };
+
+struct AttnArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* o;
+  float* lse;
+  int B, H, N, d;
+  int causal;   // 0 or 1
+  int dtype;    // 0 = fp16, 1 = bf16
+  float c;      // |scale| * log2(e), a normal positive float
+  int qmode;    // QMode
+};
+
+// Enqueues the kernel instance for (d, dtype, causal).  Arguments have been
+// validated by the caller.  Returns the HIP launch status.
+hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream);
+
+}  // namespace qm

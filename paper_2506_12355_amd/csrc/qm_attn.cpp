@@ -1,0 +1,90 @@
+// C-ABI front end of the attention library: argument validation, the choice of
+// the Q conditioning mode for the scale, and dispatch to the gfx950 kernels.
+// The operation and every argument are documented in include/qm_attn.h.
+
+#include "qm_attn.h"
+
+#include <float.h>
+#include <limits.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "attn_fwd_launch.h"
+
+namespace {
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+  return a0 < b0 + nb && b0 < a0 + na;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+}  // namespace
+
+extern "C" int qm_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
+                           int B, int H, int N, int d, float scale, int causal,
+                           hipStream_t stream, int dtype) {
+  if (!q || !k || !v || !o || !lse) return QM_ERR_NULL;
+  if (B < 1 || H < 1 || N < 1) return QM_ERR_SHAPE;
+  if (d != 64 && d != 128) return QM_ERR_HEADDIM;
+  // element counts: the whole tensor in 62 bits, one head's [N][d] slab and the
+  // workgroup count in 31 bits (the kernels index within a head in 32 bits)
+  const uint64_t bh = (uint64_t)B * (uint64_t)H;
+  const uint64_t nd = (uint64_t)N * (uint64_t)d;
+  if (nd >= (1ull << 31) || bh >= (1ull << 62) / nd) return QM_ERR_SHAPE;
+  if ((uint64_t)((N + 127) / 128) * bh > (uint64_t)INT_MAX) return QM_ERR_SHAPE;
+  if (dtype != QM_F16 && dtype != QM_BF16) return QM_ERR_DTYPE;
+  if (!isfinite(scale)) return QM_ERR_SCALE;
+  if (causal != 0 && causal != 1) return QM_ERR_CAUSAL;
+
+  const size_t tensor_bytes = (size_t)(bh * nd) * 2;
+  const size_t lse_bytes = (size_t)(bh * (uint64_t)N) * sizeof(float);
+  if (overlaps(o, tensor_bytes, q, tensor_bytes) || overlaps(o, tensor_bytes, k, tensor_bytes) ||
+      overlaps(o, tensor_bytes, v, tensor_bytes) || overlaps(lse, lse_bytes, q, tensor_bytes) ||
+      overlaps(lse, lse_bytes, k, tensor_bytes) || overlaps(lse, lse_bytes, v, tensor_bytes) ||
+      overlaps(lse, lse_bytes, o, tensor_bytes))
+    return QM_ERR_ALIAS;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse))
+    return QM_ERR_UNSUPPORTED;
+
+  qm::AttnArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.o = static_cast<uint16_t*>(o);
+  a.lse = lse;
+  a.B = B;
+  a.H = H;
+  a.N = N;
+  a.d = d;
+  a.causal = causal;
+  a.dtype = dtype;
+  // exp2-domain scale; the sign goes into Q (exact), a zero or negligible
+  // scale becomes all-zero scores (exact: every visible score is 0)
+  const double c = fabs((double)scale) * 1.4426950408889634074;
+  a.c = (float)c;
+  if (!(a.c >= FLT_MIN)) {
+    a.c = 1.0f;
+    a.qmode = qm::kQZero;
+  } else {
+    a.qmode = scale < 0.0f ? qm::kQNegate : qm::kQNormal;
+  }
+  return qm::launch_attn_fwd(a, stream) == hipSuccess ? QM_OK : QM_ERR_LAUNCH;
+}
+
+extern "C" const char* qm_attn_strerror(int status) {
+  switch (status) {
+    case QM_OK: return "success";
+    case QM_ERR_NULL: return "a tensor pointer is NULL";
+    case QM_ERR_SHAPE: return "B, H or N is below 1, or the tensors are too large";
+    case QM_ERR_HEADDIM: return "head dimension d must be 64 or 128";
+    case QM_ERR_DTYPE: return "dtype must be QM_F16 (0) or QM_BF16 (1)";
+    case QM_ERR_SCALE: return "scale must be finite";
+    case QM_ERR_ALIAS: return "o or lse overlaps an input or each other";
+    case QM_ERR_CAUSAL: return "causal must be 0 or 1";
+    case QM_ERR_LAUNCH: return "the HIP runtime rejected the kernel launch";
+    case QM_ERR_UNSUPPORTED: return "tensor pointers must be 16-byte aligned";
+  }
+  return "unknown status";
+}
