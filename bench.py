@@ -1,0 +1,228 @@
+"""Throughput of the fused attention forward on one MI355X.
+
+Workload: B=2, H=32, N=8192, d=128, bf16, Q/K/V i.i.d. N(0,1) (seed 0),
+scale = 1/sqrt(d).  One step = one unmasked forward plus one causal forward
+over that batch (the two runs the workload is quoted on).  Inputs are resident
+in HBM before the timed region starts.
+
+Metric: TFLOPS with the paper's count, 4*B*H*N^2*d per forward (Evaluation
+section, "Benchmark setting"), halved for the causal run, summed over the
+step and divided by the wall time of the step.
+
+Prints one JSON line.  Extra objects:
+  roofline      the dominant kernel (the unmasked forward): its algorithmic
+                flops per launch over its mean launch duration, timed with
+                HIP events on the launch stream inside the timed region,
+                against the dense bf16 MFMA peak; ``traffic`` is the HBM bytes
+                per launch from rocprofv3 FETCH_SIZE + WRITE_SIZE counters
+                (scaled by a plain copy of known size), read from the
+                committed profile summary, or null once the kernel source has
+                changed since those counters were taken;
+  cpu_baseline  the fp64 CPU oracle timed on this host on a bounded sample of
+                the same workload (whole heads, both masks), in the same unit.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import seeded_inputs as si  # noqa: E402
+
+METRIC = "attention fwd TFLOPS (4·B·H·N²·d, ½ if causal) and % of MFMA peak"
+PEAK_TFLOPS = 2500.0          # MI355X dense bf16/fp16 MFMA, published
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2506_12355_amd", "csrc", "attn_fwd_gfx950.hip")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_fwd_bf16_d128_n8192_hbm_traffic.md")
+
+
+def flops(B, H, N, d, causal):
+    f = 4.0 * B * H * N * N * d
+    return f / 2 if causal else f
+
+
+def kernel_source_sha256() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def committed_traffic():
+    """HBM bytes per unmasked launch from the committed counter summary, if current."""
+    if not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    text = open(TRAFFIC_SUMMARY).read()
+    sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
+    val = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not sha or not val or sha.group(1) != kernel_source_sha256():
+        return None
+    return float(val.group(1))
+
+
+# --------------------------------------------------------------------------
+# CPU baseline: the fp64 oracle on whole heads of the same workload
+# --------------------------------------------------------------------------
+def _oracle_head(args):
+    from threadpoolctl import threadpool_limits
+    from oracle import attention_fp64
+    q, k, v, scale, dtype = args
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        for causal in (False, True):
+            attention_fp64(q, k, v, scale, causal, dtype)
+        return time.perf_counter() - t0
+
+
+def cpu_baseline(w, q, k, v, max_workers=16):
+    import multiprocessing as mp
+    cores = max(1, min(max_workers, len(os.sched_getaffinity(0))))
+    n_heads = min(w.B * w.H, 4 * cores)
+    heads = [(i // w.H, i % w.H) for i in range(n_heads)]
+    jobs = [(q[b:b + 1, h:h + 1].copy(), k[b:b + 1, h:h + 1].copy(),
+             v[b:b + 1, h:h + 1].copy(), w.scale, w.dtype) for b, h in heads]
+    ctx = mp.get_context("fork")
+    t0 = time.perf_counter()
+    with ctx.Pool(cores) as pool:
+        pool.map(_oracle_head, jobs, chunksize=1)
+    wall = time.perf_counter() - t0
+    work = len(heads) * (flops(1, 1, w.N, w.d, False) + flops(1, 1, w.N, w.d, True))
+    return {
+        "value": round(work / wall / 1e12, 6),
+        "unit": "TFLOPS",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": (f"{len(heads)} of {w.B * w.H} (batch, head) slices of {w.name}, both masks, "
+                   f"spread over {cores} processes with single-threaded BLAS; wall {wall:.1f} s"),
+    }
+
+
+# --------------------------------------------------------------------------
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the CPU oracle leg (for profiler runs)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB device copy (HBM counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the attention forward shards over heads without communication, "
+              "so per-GPU throughput is the single-GPU figure)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2506_12355_amd as qa
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a ROCm GPU", file=sys.stderr)
+        sys.exit(1)
+    qa.load_library()
+
+    w = si.WORKLOADS[si.BENCH_WORKLOAD]
+    q, k, v = w.inputs()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    def dev16(x):
+        return torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+
+    tq, tk, tv = dev16(q), dev16(k), dev16(v)
+    o_nc = torch.empty_like(tq)
+    o_c = torch.empty_like(tq)
+    l_nc = torch.empty((w.B, w.H, w.N), dtype=torch.float32, device=dev)
+    l_c = torch.empty_like(l_nc)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        qa.fwd(tq, tk, tv, causal=False, scale=w.scale, out=o_nc, lse=l_nc, stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        qa.fwd(tq, tk, tv, causal=True, scale=w.scale, out=o_c, lse=l_c, stream=stream)
+        if ev is not None:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize(dev)
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)]
+              for _ in range(args.steps)]
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - t0
+
+    nc_ms = [e[0].elapsed_time(e[1]) for e in events]
+    c_ms = [e[1].elapsed_time(e[2]) for e in events]
+    f_nc = flops(w.B, w.H, w.N, w.d, False)
+    f_c = flops(w.B, w.H, w.N, w.d, True)
+    ms_per_step = wall * 1e3 / args.steps
+    value = (f_nc + f_c) / (ms_per_step * 1e-3) / 1e12
+    nc_mean = sum(nc_ms) / len(nc_ms)
+    c_mean = sum(c_ms) / len(c_ms)
+    achieved = f_nc / (nc_mean * 1e-3) / 1e12
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 29, dtype=torch.int16, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize(dev)
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{w.name}: unmasked + causal forward per step",
+            "B": w.B, "H": w.H, "N": w.N, "d": w.d, "dtype": w.dtype,
+            "masks": ["none", "causal"], "seed": w.seed,
+        },
+        "pct_of_peak": round(100.0 * value / PEAK_TFLOPS, 2),
+        "per_launch": {
+            "unmasked": {"ms": round(nc_mean, 4), "tflops": round(achieved, 2)},
+            "causal": {"ms": round(c_mean, 4),
+                       "tflops": round(f_c / (c_mean * 1e-3) / 1e12, 2)},
+        },
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "attn_fwd_kernel<128, bf16, unmasked>",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_TFLOPS, 4),
+            "traffic": committed_traffic(),
+        },
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, q, k, v)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
