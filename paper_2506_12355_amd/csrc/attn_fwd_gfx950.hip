@@ -8,33 +8,37 @@
 // wavefronts own 32 rows each and walk the key/value sequence in blocks of
 // BN = 64 keys (the loop of the paper's Appendix B listings).
 //
-// The two products are arranged for the 32x32x16 MFMA of CDNA4:
+// The two products use the 32x32x16 MFMA of CDNA4:
 //
 //   GEMM-I   S^T[key][query] = K[key][:] . Q[query][:]
 //            A operand = K rows read from LDS (K keeps its stored layout, the
 //            point of the paper's "GEMM error" case), B operand = Q, loaded
-//            once from HBM and resident in VGPRs.  The accumulator gives each
-//            lane one query column, so the row max / row sum of a query are an
-//            in-register reduction plus one exchange between the two lane
-//            halves that share the column.
+//            once and resident in VGPRs.  The accumulator gives each lane one
+//            query column, so a query's row max / row sum is an in-register
+//            reduction plus one swap between the two lane halves sharing the
+//            column (v_permlane32_swap).
 //
 //   GEMM-II  O^T[d][query] += V^T[d][key] . P^T[key][query]
-//            B operand = P^T, taken straight from the GEMM-I accumulator
-//            registers after an fp32 -> 16-bit pack.  This is the paper's
-//            "Reshape S from MMA_C to MMA_A" step, done without moving data:
-//            the accumulator holds, per lane half, keys {0-3, 8-11, ...} or
-//            {4-7, 12-15, ...}; V^T is stored in LDS with bits 2 and 3 of the
-//            key index swapped, so one 128-bit LDS read returns exactly the
-//            keys whose probabilities the lane holds.  The contraction order
-//            over keys is free, so nothing else changes.
+//            B operand = P^T, taken straight from the GEMM-I accumulator after
+//            an fp32 -> 16-bit pack.  This is the paper's "Reshape S from
+//            MMA_C to MMA_A" step, done without moving data: per lane half the
+//            accumulator holds keys {0-3, 8-11, ...} or {4-7, 12-15, ...}, and
+//            the A operand V^T is gathered from row-major V in LDS with the
+//            transposing read ds_read_b64_tr_b16 (within each 16-lane group,
+//            output lane i, slot r takes element i%4 of source lane 4r + i/4),
+//            pointing its four lane quads at exactly those four key rows.  The
+//            contraction order over keys is free, so nothing else changes.
 //
-// K/V staging: the next key block is fetched from HBM into registers with
-// 128-bit loads while the current block is consumed from LDS, then written to
-// the other LDS buffer (two buffers, one barrier per block).  V is transposed
-// on the way in (4 keys x 8 dims per thread, 64-bit LDS writes).
+// K/V staging: each key block goes HBM -> LDS with direct buffer loads
+// (buffer_load_dwordx4 ... lds; lane l's 16 bytes land at M0 + 16 l), issued
+// one block ahead into the other of two LDS buffers; one barrier per block.
+// Rows past the end of the sequence read as zeros (buffer range checking), so
+// no load needs a branch.  16-byte units are XOR-swizzled per row so that the
+// 128-bit K reads (16 rows, one column of units) and the transposing V reads
+// (4 rows x 4 units) each hit 16 distinct bank groups.
 //
 // Online softmax (exp2 domain, c = |scale| * log2 e):
-//   m_blk = c * max_j s_j;   p_j = 2^(c*s_j - m);   l += sum_j p_j
+//   m_blk = c * max_j s_j;   p_j = 2^(c*s_j - m);   l += sum_j p_j (fp32)
 //   The running maximum m is only raised when a block's maximum exceeds it by
 //   more than TAU = 8 (then O and l are rescaled by 2^(m_old - m_new)).  The
 //   result is exact for any m not below the true maximum minus TAU: every p_j
@@ -67,6 +71,10 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 
 constexpr int kBM = 128;      // query rows per workgroup
 constexpr int kBN = 64;       // keys per block
@@ -74,6 +82,10 @@ constexpr int kWaves = 4;     // 32 query rows per wavefront
 constexpr int kThreads = 64 * kWaves;
 constexpr float kTau = 8.0f;  // lazy-rescale threshold (log2 units)
 constexpr int kXcds = 8;
+constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data
+// s_waitcnt immediate for vmcnt(0) and lgkmcnt(0): the direct LDS loads of
+// this wave have landed
+constexpr int kWaitLoads = 0x0070;
 
 struct KParams {
   const uint16_t* q;
@@ -88,7 +100,8 @@ struct KParams {
   int qmode;
 };
 
-// 16-bit type traits: the MFMA and the fp32 -> 16-bit pack (round to nearest even).
+// 16-bit type traits: the MFMA and the fp32 -> 16-bit pack (round to nearest
+// even).
 template <int DT>
 struct Half;
 
@@ -114,29 +127,61 @@ struct Half<1> {  // bf16
   }
 };
 
-// Position of key k inside a V^T row of LDS: bits 2 and 3 swapped (an involution).
-__device__ __forceinline__ int vt_pos(int k) {
-  return (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1);
+// Per-row XOR swizzles of 16-byte units (U units per row).
+//   K: rows r..r+15 read the same unit column -> r & 15 (U = 16), or
+//      (r >> 1) & 7 with the row parity as the extra bank bit (U = 8).
+//   V: transposing reads touch 4 rows x 4 consecutive units -> flip bits 2..3
+//      of the unit index by the row within its group of four.
+template <int U>
+__device__ __forceinline__ int swz_k(int r) {
+  return U == 16 ? (r & 15) : ((r >> 1) & 7);
+}
+template <int U>
+__device__ __forceinline__ int swz_v(int r) {
+  return U == 16 ? 4 * (r & 3) : 4 * ((r >> 1) & 1);
 }
 
-__device__ __forceinline__ u32x4 ld16(const uint16_t* p) {
-  return *reinterpret_cast<const u32x4*>(p);
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kRsrcWord3);
+}
+
+// Exchange between the two lane halves that share a query column:
+// v_permlane32_swap(a, b) swaps a's upper 32 lanes with b's lower 32 lanes, so
+// with a = b = x, lane i < 32 ends with (x_i, x_{i+32}) and lane i >= 32 with
+// (x_{i-32}, x_i): own and partner value in every lane.  The two results are
+// copied to scalars before any bit cast (a bit cast applied to an element of
+// the returned vector reads element 0).
+__device__ __forceinline__ float max_across_halves(float x) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const uint32_t a = r[0], b = r[1];
+  return fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
+}
+
+__device__ __forceinline__ float sum_across_halves(float x) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const uint32_t a = r[0], b = r[1];
+  return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
+}
+
+// One 16-byte-per-lane direct load HBM -> LDS (lane l lands at lds + 16 l).
+// Kept out of the kernel body: used there directly, the builtin makes the host
+// pass drop the kernels' launch stubs.
+__device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t rs, void* lds, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)lds, 16, voff, 0, 0, 0);
 }
 
 template <int D, int DT, bool CAUSAL>
 __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
-  constexpr int KSTR = D + 8;         // LDS row stride of K (halfs): 4 banks of skew per row
-  constexpr int VSTR = kBN + 8;       // LDS row stride of V^T (halfs)
-  constexpr int KTILE = kBN * KSTR;
-  constexpr int VTILE = D * VSTR;
-  constexpr int BUF = KTILE + VTILE;
-  constexpr int DCH = D / 8;                      // 16-byte chunks per row
-  constexpr int KCH = kBN * DCH / kThreads;       // K chunks per thread per block
-  constexpr int VTASKS = (kBN / 4) * DCH;         // (4 keys x 8 dims) V tasks per block
+  constexpr int U = D / 8;                        // 16-byte units per row
+  constexpr int TILE = kBN * D;                   // 16-bit elements per K or V tile
+  constexpr int BUF = 2 * TILE;                   // K tile then V tile
+  constexpr int ROWS_PER_LOAD = 64 / U;           // rows written by one 1 KB direct load
+  constexpr int LOADS_PER_WAVE = kBN / ROWS_PER_LOAD / kWaves;
   constexpr int NKS = D / 16;                     // GEMM-I k-steps
   constexpr int NMT = D / 32;                     // GEMM-II M tiles
-  static_assert(KCH * kThreads == kBN * DCH, "K staging must tile the block");
-  static_assert(VTASKS <= kThreads, "one V task per thread at most");
+  static_assert(LOADS_PER_WAVE * kWaves * ROWS_PER_LOAD == kBN, "loads must tile a block");
 
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
 
@@ -156,9 +201,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
   if (CAUSAL) qb = p.nq - 1 - qb;  // longest rows first
 
   const size_t head = (size_t)bh * (size_t)N * D;
-  const uint16_t* __restrict__ Qh = p.q + head;
-  const uint16_t* __restrict__ Kh = p.k + head;
-  const uint16_t* __restrict__ Vh = p.v + head;
+  const uint32_t head_bytes = (uint32_t)N * D * 2;
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + head, head_bytes);
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(p.k + head, head_bytes);
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(p.v + head, head_bytes);
 
   const int q0 = qb * kBM;
   const int qw = q0 + wave * 32;   // first query row of this wavefront
@@ -168,7 +214,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
   u32x4 qf[NKS];
 #pragma unroll
   for (int ks = 0; ks < NKS; ++ks) {
-    qf[ks] = (qrow < N) ? ld16(Qh + (size_t)qrow * D + 16 * ks + 8 * hi) : u32x4{0, 0, 0, 0};
+    qf[ks] = __builtin_amdgcn_raw_buffer_load_b128(rq, (uint32_t)(qrow * D + 16 * ks + 8 * hi) * 2, 0, 0);
     if (p.qmode == kQNegate) qf[ks] ^= 0x80008000u;
     if (p.qmode == kQZero) qf[ks] = u32x4{0, 0, 0, 0};
   }
@@ -182,60 +228,56 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
   float m_run = -INFINITY;   // running maximum, exp2 domain
   float l_run = 0.f;         // this lane's share of the running row sum
 
-  // ---- HBM -> register staging of one key block ----
-  u32x4 kst[KCH];
-  u32x4 vst[4];
-  const int vkg = tid / DCH;   // V task: keys 4*vkg .. 4*vkg+3
-  const int vdc = tid % DCH;   //         dims 8*vdc .. 8*vdc+7
-  const bool vtask = (VTASKS == kThreads) || (tid < VTASKS);
-
-  auto gload = [&](int j0) {
+  // ---- HBM -> LDS: this wave's share of one key block, straight into LDS ----
+  auto load_block = [&](int j0, int buf) {
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int c = tid + kThreads * i;
-      const int row = j0 + c / DCH;
-      kst[i] = (row < N) ? ld16(Kh + (size_t)row * D + 8 * (c % DCH)) : u32x4{0, 0, 0, 0};
-    }
-    if (vtask) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = j0 + 4 * vkg + i;
-        vst[i] = (row < N) ? ld16(Vh + (size_t)row * D + 8 * vdc) : u32x4{0, 0, 0, 0};
-      }
+    for (int i = 0; i < LOADS_PER_WAVE; ++i) {
+      const int chunk = wave * LOADS_PER_WAVE + i;          // 1 KB chunk of the tile
+      const int r = chunk * ROWS_PER_LOAD + lane / U;       // tile row this lane fills
+      const int pos = lane % U;                             // its unit position in the row
+      const uint32_t row_off = (uint32_t)((j0 + r) * D) * 2;
+      uint16_t* kdst = smem + buf * BUF + chunk * 512;
+      uint16_t* vdst = kdst + TILE;
+      lds_load16(rk, kdst, row_off + 16 * (pos ^ swz_k<U>(r)));
+      lds_load16(rv, vdst, row_off + 16 * (pos ^ swz_v<U>(r)));
     }
   };
 
-  auto swrite = [&](int buf) {
-    uint16_t* Ks = smem + buf * BUF;
-    uint16_t* Vs = Ks + KTILE;
+  // per-lane LDS element offsets of the operand reads (within one buffer)
+  int k_off[2][NKS];
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int c = tid + kThreads * i;
-      *reinterpret_cast<u32x4*>(Ks + (c / DCH) * KSTR + 8 * (c % DCH)) = kst[i];
+  for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      const int r = 32 * kt + l32;
+      k_off[kt][ks] = (r * U + ((2 * ks + hi) ^ swz_k<U>(r))) * 8;
     }
-    if (vtask) {
-      const int pos = vt_pos(4 * vkg);
+  }
+  const int grp = lane >> 4;       // 16-lane group of the transposing read
+  const int sl = lane & 15;
+  int v_off[NMT][4][2];
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {   // dims 8*vdc + 2w (low halves) and + 2w + 1 (high halves)
-        const uint32_t a0 = vst[0][w], a1 = vst[1][w], a2 = vst[2][w], a3 = vst[3][w];
-        const u32x2 ev = {(a0 & 0xFFFFu) | (a1 << 16), (a2 & 0xFFFFu) | (a3 << 16)};
-        const u32x2 od = {(a0 >> 16) | (a1 & 0xFFFF0000u), (a2 >> 16) | (a3 & 0xFFFF0000u)};
-        *reinterpret_cast<u32x2*>(Vs + (8 * vdc + 2 * w) * VSTR + pos) = ev;
-        *reinterpret_cast<u32x2*>(Vs + (8 * vdc + 2 * w + 1) * VSTR + pos) = od;
+  for (int mt = 0; mt < NMT; ++mt) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        const int key = 16 * u + 8 * h2 + 4 * (grp >> 1) + (sl >> 2);
+        const int d0 = 32 * mt + 16 * (grp & 1) + 4 * (sl & 3);
+        v_off[mt][u][h2] = TILE + (key * U + ((d0 >> 3) ^ swz_v<U>(key))) * 8 + (d0 & 7);
       }
     }
-  };
+  }
 
-  gload(0);
-  swrite(0);
+  load_block(0, 0);
+  __builtin_amdgcn_s_waitcnt(kWaitLoads);
   __syncthreads();
 
   for (int j = 0; j < nkv; ++j) {
     const int j0 = j * kBN;
-    if (j + 1 < nkv) gload(j0 + kBN);
+    if (j + 1 < nkv) load_block(j0 + kBN, (j + 1) & 1);
 
-    const uint16_t* Ks = smem + (j & 1) * BUF;
-    const uint16_t* Vs = Ks + KTILE;
+    const uint16_t* buf = smem + (j & 1) * BUF;
     const bool active = (qw < N) && (!CAUSAL || j0 <= qw + 31);
     if (active) {
       // GEMM-I: two 32-key tiles of S^T
@@ -244,7 +286,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
       for (int ks = 0; ks < NKS; ++ks) {
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
-          const u32x4 a = *reinterpret_cast<const u32x4*>(Ks + (32 * kt + l32) * KSTR + 16 * ks + 8 * hi);
+          const u32x4 a = *reinterpret_cast<const u32x4*>(buf + k_off[kt][ks]);
           s[kt] = Half<DT>::mfma(a, qf[ks], s[kt]);
         }
       }
@@ -263,14 +305,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
       }
 
       // block row maximum: 32 values in-lane, then the other lane half
-      float mx = s[0][0];
+      float mx = fmaxf(s[0][0], s[1][0]);
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kt][r]);
-      }
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_blk = mx * p.c;
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s[0][r], s[1][r]));
+      const float m_blk = max_across_halves(mx) * p.c;
 
       const bool need = m_blk > m_run + kTau;
       if (__any(need)) {
@@ -283,63 +321,68 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
       }
       const float mu = (m_run == -INFINITY) ? 0.f : m_run;
 
-      // probabilities, row-sum share, and the 16-bit P^T operands
-      float lsum = 0.f;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          s[kt][r] = __builtin_amdgcn_exp2f(fmaf(s[kt][r], p.c, -mu));
-          lsum += s[kt][r];
-        }
-      }
-      l_run += lsum;
-
+      // probabilities -> 16-bit P^T operands; the row sum stays in fp32 (a sum
+      // of the rounded values would carry their rounding into lse whenever a
+      // few keys dominate the row)
       u32x4 pb[4];
+      float lsum = 0.f;
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
-          pb[u][w] = Half<DT>::pack(s[u / 2][8 * (u % 2) + 2 * w], s[u / 2][8 * (u % 2) + 2 * w + 1]);
+          const int r0 = 8 * (u % 2) + 2 * w;
+          const float e0 = __builtin_amdgcn_exp2f(fmaf(s[u / 2][r0], p.c, -mu));
+          const float e1 = __builtin_amdgcn_exp2f(fmaf(s[u / 2][r0 + 1], p.c, -mu));
+          pb[u][w] = Half<DT>::pack(e0, e1);
+          lsum += e0 + e1;
         }
       }
+      l_run += lsum;
 
-      // GEMM-II: O^T += V^T P^T
+      // GEMM-II: O^T += V^T P^T, V^T gathered by transposing LDS reads
 #pragma unroll
       for (int mt = 0; mt < NMT; ++mt) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const u32x4 a = *reinterpret_cast<const u32x4*>(Vs + (32 * mt + l32) * VSTR + 16 * u + 8 * hi);
+          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + v_off[mt][u][0]));
+          const i16x4 hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + v_off[mt][u][1]));
+          const u32x2 a0 = __builtin_bit_cast(u32x2, lo);
+          const u32x2 a1 = __builtin_bit_cast(u32x2, hi4);
+          const u32x4 a = {a0[0], a0[1], a1[0], a1[1]};
           oacc[mt] = Half<DT>::mfma(a, pb[u], oacc[mt]);
         }
       }
     }
 
-    if (j + 1 < nkv) swrite((j + 1) & 1);
+    // this wave's loads of the next block are in LDS; after the barrier every
+    // wave's are, and every wave is done reading the current buffer
+    __builtin_amdgcn_s_waitcnt(kWaitLoads);
     __syncthreads();
   }
 
   // ---- epilogue: O = O / l in the storage type, lse in natural log ----
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (qrow < N) {
-    const float inv = 1.0f / l_tot;
-    uint16_t* Orow = p.o + head + (size_t)qrow * D;
+  const float l_tot = sum_across_halves(l_run);
+  const float inv = 1.0f / l_tot;
+  const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.o + head, head_bytes);
 #pragma unroll
-    for (int mt = 0; mt < NMT; ++mt) {
+  for (int mt = 0; mt < NMT; ++mt) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const u32x2 w = {Half<DT>::pack(oacc[mt][4 * g] * inv, oacc[mt][4 * g + 1] * inv),
-                         Half<DT>::pack(oacc[mt][4 * g + 2] * inv, oacc[mt][4 * g + 3] * inv)};
-        *reinterpret_cast<u32x2*>(Orow + 32 * mt + 8 * g + 4 * hi) = w;
-      }
+    for (int g = 0; g < 4; ++g) {
+      const u32x2 w = {Half<DT>::pack(oacc[mt][4 * g] * inv, oacc[mt][4 * g + 1] * inv),
+                       Half<DT>::pack(oacc[mt][4 * g + 2] * inv, oacc[mt][4 * g + 3] * inv)};
+      __builtin_amdgcn_raw_buffer_store_b64(w, ro, (uint32_t)(qrow * D + 32 * mt + 8 * g + 4 * hi) * 2, 0, 0);
     }
-    if (hi == 0) p.lse[(size_t)bh * N + qrow] = (m_run + log2f(l_tot)) * 0.69314718055994531f;
+  }
+  if (hi == 0) {
+    const __amdgpu_buffer_rsrc_t rl = make_rsrc(p.lse + (size_t)bh * N, (uint32_t)N * 4);
+    const float lse = (m_run + log2f(l_tot)) * 0.69314718055994531f;
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, lse), rl, (uint32_t)qrow * 4, 0, 0);
   }
 }
 
 template <int D>
 constexpr size_t lds_bytes() {
-  return 2 * (size_t)(kBN * (D + 8) + D * (kBN + 8)) * sizeof(uint16_t);
+  return 2 * 2 * (size_t)kBN * D * sizeof(uint16_t);
 }
 
 template <int D, int DT, bool CAUSAL>

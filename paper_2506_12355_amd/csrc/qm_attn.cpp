@@ -32,7 +32,9 @@ extern "C" int qm_attn_fwd(const void* q, const void* k, const void* v, void* o,
   // workgroup count in 31 bits (the kernels index within a head in 32 bits)
   const uint64_t bh = (uint64_t)B * (uint64_t)H;
   const uint64_t nd = (uint64_t)N * (uint64_t)d;
-  if (nd >= (1ull << 31) || bh >= (1ull << 62) / nd) return QM_ERR_SHAPE;
+  // a head's byte offsets, including the padded last query block, fit in 32 bits
+  if ((uint64_t)(N + 128) * (uint64_t)d >= (1ull << 31) || bh >= (1ull << 62) / nd)
+    return QM_ERR_SHAPE;
   if ((uint64_t)((N + 127) / 128) * bh > (uint64_t)INT_MAX) return QM_ERR_SHAPE;
   if (dtype != QM_F16 && dtype != QM_BF16) return QM_ERR_DTYPE;
   if (!isfinite(scale)) return QM_ERR_SCALE;

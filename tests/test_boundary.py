@@ -49,6 +49,14 @@ def test_library_exports_every_declared_symbol(lib):
         assert hasattr(lib, name)
 
 
+def test_library_has_no_undefined_kernel_symbols(lib):
+    """Every kernel's host launch stub is defined in the library itself."""
+    out = subprocess.run(["nm", "-D", "--undefined-only", qa.LIB_PATH],
+                         capture_output=True, text=True, check=True).stdout
+    missing = [line.split()[-1] for line in out.splitlines() if "qm" in line]
+    assert not missing, f"undefined symbols from the library's own code: {missing}"
+
+
 # fake, well-separated, 256-byte aligned device addresses: never dereferenced
 GIB = 1 << 30
 Q, K, V, O, L = (GIB * i for i in range(1, 6))
