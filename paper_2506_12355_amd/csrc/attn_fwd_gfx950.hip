@@ -58,6 +58,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "attn_fwd_launch.h"
 
 namespace qm {
@@ -127,19 +129,28 @@ struct Half<1> {  // bf16
   }
 };
 
-// Per-row XOR swizzles of 16-byte units (U units per row).
-//   K: rows r..r+15 read the same unit column -> r & 15 (U = 16), or
-//      (r >> 1) & 7 with the row parity as the extra bank bit (U = 8).
-//   V: transposing reads touch 4 rows x 4 consecutive units -> flip bits 2..3
-//      of the unit index by the row within its group of four.
-template <int U>
-__device__ __forceinline__ int swz_k(int r) {
-  return U == 16 ? (r & 15) : ((r >> 1) & 7);
-}
-template <int U>
-__device__ __forceinline__ int swz_v(int r) {
-  return U == 16 ? 4 * (r & 3) : 4 * ((r >> 1) & 1);
-}
+// LDS layout of one K or V tile (kBN rows of D 16-bit values).  One direct
+// load writes 1 KB = RPL whole rows; load group g holds rows g, g + NG,
+// g + 2 NG, ... (NG groups), and groups are padded: K by 16 bytes, V by 64
+// bytes.  Then a 128-bit K read of 16 consecutive rows in one column, and a
+// transposing V read of 4 consecutive rows x 4 consecutive 16-byte units,
+// each touch 16 distinct bank groups, and every operand address is a per-lane
+// base plus a compile-time offset.
+template <int D>
+struct Layout {
+  static constexpr int U = D / 8;                 // 16-byte units per row
+  static constexpr int ROW = 16 * U;              // bytes per row
+  static constexpr int RPL = 64 / U;              // rows per 1 KB load
+  static constexpr int NG = kBN / RPL;            // load groups per tile
+  static constexpr int KGS = 1024 + 16;           // K group stride (bytes)
+  static constexpr int VGS = 1024 + 64;           // V group stride (bytes)
+  static constexpr int KBYTES = NG * KGS;
+  static constexpr int VBYTES = NG * VGS;
+  static constexpr int BUF = KBYTES + VBYTES;     // one K tile + one V tile
+  static_assert(NG % kWaves == 0, "each wave issues whole load groups");
+  static_assert(NG >= 8, "a transposing read's 8 key rows must fall in distinct groups");
+  static_assert(BUF % 16 == 0, "buffers stay 16-byte aligned");
+};
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kRsrcWord3);
@@ -165,29 +176,27 @@ __device__ __forceinline__ float sum_across_halves(float x) {
   return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
 }
 
-// One 16-byte-per-lane direct load HBM -> LDS (lane l lands at lds + 16 l).
-// Kept out of the kernel body: used there directly, the builtin makes the host
-// pass drop the kernels' launch stubs.
-__device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t rs, void* lds, uint32_t voff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)lds, 16, voff, 0, 0, 0);
+// One 16-byte-per-lane direct load HBM -> LDS: lane l's bytes at
+// voff + soff of the buffer land at lds + 16 l.  Kept out of the kernel body:
+// used there directly, the builtin makes the host pass drop the kernels'
+// launch stubs.
+__device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t rs, void* lds, uint32_t voff,
+                                           uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)lds, 16, voff, soff, 0, 0);
 }
 
 template <int D, int DT, bool CAUSAL>
 __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
-  constexpr int U = D / 8;                        // 16-byte units per row
-  constexpr int TILE = kBN * D;                   // 16-bit elements per K or V tile
-  constexpr int BUF = 2 * TILE;                   // K tile then V tile
-  constexpr int ROWS_PER_LOAD = 64 / U;           // rows written by one 1 KB direct load
-  constexpr int LOADS_PER_WAVE = kBN / ROWS_PER_LOAD / kWaves;
-  constexpr int NKS = D / 16;                     // GEMM-I k-steps
-  constexpr int NMT = D / 32;                     // GEMM-II M tiles
-  static_assert(LOADS_PER_WAVE * kWaves * ROWS_PER_LOAD == kBN, "loads must tile a block");
+  using L = Layout<D>;
+  constexpr int NKS = D / 16;          // GEMM-I k-steps
+  constexpr int NMT = D / 32;          // GEMM-II M tiles
+  constexpr int GPW = L::NG / kWaves;  // load groups per wave per tile
 
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+  char* const lds = reinterpret_cast<char*>(smem);
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l32 = lane & 31;
   const int hi = lane >> 5;
   const int N = p.N;
@@ -228,56 +237,47 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
   float m_run = -INFINITY;   // running maximum, exp2 domain
   float l_run = 0.f;         // this lane's share of the running row sum
 
-  // ---- HBM -> LDS: this wave's share of one key block, straight into LDS ----
+  // ---- HBM -> LDS: this wave's load groups of one key block ----
+  // lane part of the global offset (row slot, 16-byte unit); the rest is uniform
+  const uint32_t load_lane_off = (uint32_t)(L::NG * (lane / L::U) * D * 2 + (lane % L::U) * 16);
   auto load_block = [&](int j0, int buf) {
 #pragma unroll
-    for (int i = 0; i < LOADS_PER_WAVE; ++i) {
-      const int chunk = wave * LOADS_PER_WAVE + i;          // 1 KB chunk of the tile
-      const int r = chunk * ROWS_PER_LOAD + lane / U;       // tile row this lane fills
-      const int pos = lane % U;                             // its unit position in the row
-      const uint32_t row_off = (uint32_t)((j0 + r) * D) * 2;
-      uint16_t* kdst = smem + buf * BUF + chunk * 512;
-      uint16_t* vdst = kdst + TILE;
-      lds_load16(rk, kdst, row_off + 16 * (pos ^ swz_k<U>(r)));
-      lds_load16(rv, vdst, row_off + 16 * (pos ^ swz_v<U>(r)));
+    for (int i = 0; i < GPW; ++i) {
+      const int g = wave * GPW + i;
+      const uint32_t soff = (uint32_t)((j0 + g) * D) * 2;
+      lds_load16(rk, lds + buf * L::BUF + g * L::KGS, load_lane_off, soff);
+      lds_load16(rv, lds + buf * L::BUF + L::KBYTES + g * L::VGS, load_lane_off, soff);
     }
   };
 
-  // per-lane LDS element offsets of the operand reads (within one buffer)
-  int k_off[2][NKS];
-#pragma unroll
-  for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
-      const int r = 32 * kt + l32;
-      k_off[kt][ks] = (r * U + ((2 * ks + hi) ^ swz_k<U>(r))) * 8;
-    }
-  }
-  const int grp = lane >> 4;       // 16-lane group of the transposing read
+  // per-lane LDS byte bases of the operand reads; every read adds a constant
+  //   K (A of GEMM-I): row r = 32 kt + l32 -> group r % NG, slot r / NG; unit 2 ks + hi
+  const int k_base = (l32 % L::NG) * L::KGS + (l32 / L::NG) * L::ROW + 16 * hi;
+  //   V (A of GEMM-II, transposing read): key = 16 u + 8 h2 + kq, dims d0 .. d0+3
+  const int grp = lane >> 4;
   const int sl = lane & 15;
-  int v_off[NMT][4][2];
-#pragma unroll
-  for (int mt = 0; mt < NMT; ++mt) {
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-#pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2) {
-        const int key = 16 * u + 8 * h2 + 4 * (grp >> 1) + (sl >> 2);
-        const int d0 = 32 * mt + 16 * (grp & 1) + 4 * (sl & 3);
-        v_off[mt][u][h2] = TILE + (key * U + ((d0 >> 3) ^ swz_v<U>(key))) * 8 + (d0 & 7);
-      }
-    }
-  }
+  const int kq = 4 * (grp >> 1) + (sl >> 2);
+  const int v_base = L::KBYTES + kq * L::VGS + 2 * (16 * (grp & 1) + 4 * (sl & 3));
 
-  load_block(0, 0);
-  __builtin_amdgcn_s_waitcnt(kWaitLoads);
-  __syncthreads();
+  auto k_read = [&](const char* b, int kt, int ks) {
+    constexpr int SLOTS_PER_32 = 32 / L::NG;
+    return *reinterpret_cast<const u32x4*>(b + k_base + kt * SLOTS_PER_32 * L::ROW + 32 * ks);
+  };
+  auto v_read = [&](const char* b, int mt, int u, int h2) {
+    // group of key 16 u + 8 h2 + kq is (16 u + 8 h2) % NG + kq, slot (16 u + 8 h2) / NG
+    const int g_off = (16 * u + 8 * h2) % L::NG;
+    const int slot = (16 * u + 8 * h2) / L::NG;
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4*)(b + v_base + g_off * L::VGS + slot * L::ROW + 64 * mt));
+  };
 
-  for (int j = 0; j < nkv; ++j) {
+  // one key block: prefetch the next one into the other buffer, consume this one
+  auto step = [&](auto bufc, int j) {
+    constexpr int B = decltype(bufc)::value;
     const int j0 = j * kBN;
-    if (j + 1 < nkv) load_block(j0 + kBN, (j + 1) & 1);
+    if (j + 1 < nkv) load_block(j0 + kBN, 1 - B);
 
-    const uint16_t* buf = smem + (j & 1) * BUF;
+    const char* b = lds + B * L::BUF;
     const bool active = (qw < N) && (!CAUSAL || j0 <= qw + 31);
     if (active) {
       // GEMM-I: two 32-key tiles of S^T
@@ -285,10 +285,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) {
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-          const u32x4 a = *reinterpret_cast<const u32x4*>(buf + k_off[kt][ks]);
-          s[kt] = Half<DT>::mfma(a, qf[ks], s[kt]);
-        }
+        for (int kt = 0; kt < 2; ++kt) s[kt] = Half<DT>::mfma(k_read(b, kt, ks), qf[ks], s[kt]);
       }
 
       // mask: keys past the end of the sequence, keys after the query (causal)
@@ -344,10 +341,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
       for (int mt = 0; mt < NMT; ++mt) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + v_off[mt][u][0]));
-          const i16x4 hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + v_off[mt][u][1]));
-          const u32x2 a0 = __builtin_bit_cast(u32x2, lo);
-          const u32x2 a1 = __builtin_bit_cast(u32x2, hi4);
+          const u32x2 a0 = __builtin_bit_cast(u32x2, v_read(b, mt, u, 0));
+          const u32x2 a1 = __builtin_bit_cast(u32x2, v_read(b, mt, u, 1));
           const u32x4 a = {a0[0], a0[1], a1[0], a1[1]};
           oacc[mt] = Half<DT>::mfma(a, pb[u], oacc[mt]);
         }
@@ -355,9 +350,18 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
     }
 
     // this wave's loads of the next block are in LDS; after the barrier every
-    // wave's are, and every wave is done reading the current buffer
+    // wave's are, and every wave is done reading this buffer
     __builtin_amdgcn_s_waitcnt(kWaitLoads);
     __syncthreads();
+  };
+
+  load_block(0, 0);
+  __builtin_amdgcn_s_waitcnt(kWaitLoads);
+  __syncthreads();
+
+  for (int j = 0; j < nkv; j += 2) {
+    step(std::integral_constant<int, 0>{}, j);
+    if (j + 1 < nkv) step(std::integral_constant<int, 1>{}, j + 1);
   }
 
   // ---- epilogue: O = O / l in the storage type, lse in natural log ----
@@ -382,7 +386,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
 
 template <int D>
 constexpr size_t lds_bytes() {
-  return 2 * 2 * (size_t)kBN * D * sizeof(uint16_t);
+  return 2 * (size_t)Layout<D>::BUF;
 }
 
 template <int D, int DT, bool CAUSAL>

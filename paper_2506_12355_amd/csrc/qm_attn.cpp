@@ -8,6 +8,7 @@
 #include <limits.h>
 #include <math.h>
 #include <stdint.h>
+#include <string.h>
 
 #include "attn_fwd_launch.h"
 
@@ -19,6 +20,13 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// finite iff the exponent field is not all ones (independent of fast-math flags)
+bool finite_bits(float x) {
+  uint32_t u;
+  memcpy(&u, &x, sizeof(u));
+  return (u & 0x7F800000u) != 0x7F800000u;
+}
 
 }  // namespace
 
@@ -37,7 +45,7 @@ extern "C" int qm_attn_fwd(const void* q, const void* k, const void* v, void* o,
     return QM_ERR_SHAPE;
   if ((uint64_t)((N + 127) / 128) * bh > (uint64_t)INT_MAX) return QM_ERR_SHAPE;
   if (dtype != QM_F16 && dtype != QM_BF16) return QM_ERR_DTYPE;
-  if (!isfinite(scale)) return QM_ERR_SCALE;
+  if (!finite_bits(scale)) return QM_ERR_SCALE;
   if (causal != 0 && causal != 1) return QM_ERR_CAUSAL;
 
   const size_t tensor_bytes = (size_t)(bh * nd) * 2;
