@@ -237,16 +237,24 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
   float m_run = -INFINITY;   // running maximum, exp2 domain
   float l_run = 0.f;         // this lane's share of the running row sum
 
-  // ---- HBM -> LDS: this wave's load groups of one key block ----
+  // ---- HBM -> LDS: this wave's load groups of one K or V block ----
+  // LDS: K buffers 0 and 1, then V buffers 0 and 1
+  constexpr int VOFF = 2 * L::KBYTES;
   // lane part of the global offset (row slot, 16-byte unit); the rest is uniform
   const uint32_t load_lane_off = (uint32_t)(L::NG * (lane / L::U) * D * 2 + (lane % L::U) * 16);
-  auto load_block = [&](int j0, int buf) {
+  auto load_k = [&](int j0, int kb) {
 #pragma unroll
     for (int i = 0; i < GPW; ++i) {
       const int g = wave * GPW + i;
-      const uint32_t soff = (uint32_t)((j0 + g) * D) * 2;
-      lds_load16(rk, lds + buf * L::BUF + g * L::KGS, load_lane_off, soff);
-      lds_load16(rv, lds + buf * L::BUF + L::KBYTES + g * L::VGS, load_lane_off, soff);
+      lds_load16(rk, lds + kb * L::KBYTES + g * L::KGS, load_lane_off, (uint32_t)((j0 + g) * D) * 2);
+    }
+  };
+  auto load_v = [&](int j0, int vb) {
+#pragma unroll
+    for (int i = 0; i < GPW; ++i) {
+      const int g = wave * GPW + i;
+      lds_load16(rv, lds + VOFF + vb * L::VBYTES + g * L::VGS, load_lane_off,
+                 (uint32_t)((j0 + g) * D) * 2);
     }
   };
 
@@ -257,111 +265,158 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
   const int grp = lane >> 4;
   const int sl = lane & 15;
   const int kq = 4 * (grp >> 1) + (sl >> 2);
-  const int v_base = L::KBYTES + kq * L::VGS + 2 * (16 * (grp & 1) + 4 * (sl & 3));
+  const int v_base = VOFF + kq * L::VGS + 2 * (16 * (grp & 1) + 4 * (sl & 3));
 
-  auto k_read = [&](const char* b, int kt, int ks) {
+  auto k_read = [&](int kb, int kt, int ks) {
     constexpr int SLOTS_PER_32 = 32 / L::NG;
-    return *reinterpret_cast<const u32x4*>(b + k_base + kt * SLOTS_PER_32 * L::ROW + 32 * ks);
+    return *reinterpret_cast<const u32x4*>(lds + kb * L::KBYTES + k_base +
+                                           kt * SLOTS_PER_32 * L::ROW + 32 * ks);
   };
-  auto v_read = [&](const char* b, int mt, int u, int h2) {
+  auto v_read = [&](int vb, int mt, int u, int h2) {
     // group of key 16 u + 8 h2 + kq is (16 u + 8 h2) % NG + kq, slot (16 u + 8 h2) / NG
     const int g_off = (16 * u + 8 * h2) % L::NG;
     const int slot = (16 * u + 8 * h2) / L::NG;
     return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_i16x4*)(b + v_base + g_off * L::VGS + slot * L::ROW + 64 * mt));
+        (lds_i16x4*)(lds + vb * L::VBYTES + v_base + g_off * L::VGS + slot * L::ROW + 64 * mt));
   };
 
-  // one key block: prefetch the next one into the other buffer, consume this one
-  auto step = [&](auto bufc, int j) {
-    constexpr int B = decltype(bufc)::value;
+  // whether this wave has a visible key in block j (causal: blocks above its rows are skipped)
+  auto active = [&](int j) { return (qw < N) && (!CAUSAL || j * kBN <= qw + 31); };
+
+  // GEMM-I: two 32-key tiles of S^T for the block in K buffer kb
+  auto gemm1 = [&](int kb, f32x16 (&s)[2]) {
+    s[0] = f32x16{};
+    s[1] = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) s[kt] = Half<DT>::mfma(k_read(kb, kt, ks), qf[ks], s[kt]);
+    }
+  };
+
+  // Block j: mask, row max and (rare) rescale; then, in one straight-line
+  // region, the exponentials of block j interleaved with the MFMAs of GEMM-I
+  // for block j+1; then GEMM-II of block j.  GEMM-I always runs: on a wave's
+  // last block it reads a stale (in-bounds) K buffer and its result is dropped,
+  // which keeps a single code path and the register allocation compact.
+  auto block = [&](int j, int kb_next, int vb, f32x16 (&s)[2], f32x16 (&s_next)[2]) {
     const int j0 = j * kBN;
-    if (j + 1 < nkv) load_block(j0 + kBN, 1 - B);
-
-    const char* b = lds + B * L::BUF;
-    const bool active = (qw < N) && (!CAUSAL || j0 <= qw + 31);
-    if (active) {
-      // GEMM-I: two 32-key tiles of S^T
-      f32x16 s[2] = {f32x16{}, f32x16{}};
+    // mask: keys past the end of the sequence, keys after the query (causal)
+    const bool need_mask = (j0 + kBN > N) || (CAUSAL && j0 + kBN - 1 > qw);
+    if (need_mask) {
 #pragma unroll
-      for (int ks = 0; ks < NKS; ++ks) {
+      for (int kt = 0; kt < 2; ++kt) {
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt) s[kt] = Half<DT>::mfma(k_read(b, kt, ks), qf[ks], s[kt]);
-      }
-
-      // mask: keys past the end of the sequence, keys after the query (causal)
-      const bool need_mask = (j0 + kBN > N) || (CAUSAL && j0 + kBN - 1 > qw);
-      if (need_mask) {
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = j0 + 32 * kt + 8 * (r / 4) + 4 * hi + (r % 4);
-            if (key >= N || (CAUSAL && key > qrow)) s[kt][r] = -INFINITY;
-          }
-        }
-      }
-
-      // block row maximum: 32 values in-lane, then the other lane half
-      float mx = fmaxf(s[0][0], s[1][0]);
-#pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s[0][r], s[1][r]));
-      const float m_blk = max_across_halves(mx) * p.c;
-
-      const bool need = m_blk > m_run + kTau;
-      if (__any(need)) {
-        const float m_new = need ? m_blk : m_run;
-        const float alpha = need ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
-#pragma unroll
-        for (int mt = 0; mt < NMT; ++mt) oacc[mt] *= alpha;
-        l_run *= alpha;
-        m_run = m_new;
-      }
-      const float mu = (m_run == -INFINITY) ? 0.f : m_run;
-
-      // probabilities -> 16-bit P^T operands; the row sum stays in fp32 (a sum
-      // of the rounded values would carry their rounding into lse whenever a
-      // few keys dominate the row)
-      u32x4 pb[4];
-      float lsum = 0.f;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const int r0 = 8 * (u % 2) + 2 * w;
-          const float e0 = __builtin_amdgcn_exp2f(fmaf(s[u / 2][r0], p.c, -mu));
-          const float e1 = __builtin_amdgcn_exp2f(fmaf(s[u / 2][r0 + 1], p.c, -mu));
-          pb[u][w] = Half<DT>::pack(e0, e1);
-          lsum += e0 + e1;
-        }
-      }
-      l_run += lsum;
-
-      // GEMM-II: O^T += V^T P^T, V^T gathered by transposing LDS reads
-#pragma unroll
-      for (int mt = 0; mt < NMT; ++mt) {
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const u32x2 a0 = __builtin_bit_cast(u32x2, v_read(b, mt, u, 0));
-          const u32x2 a1 = __builtin_bit_cast(u32x2, v_read(b, mt, u, 1));
-          const u32x4 a = {a0[0], a0[1], a1[0], a1[1]};
-          oacc[mt] = Half<DT>::mfma(a, pb[u], oacc[mt]);
+        for (int r = 0; r < 16; ++r) {
+          const int key = j0 + 32 * kt + 8 * (r / 4) + 4 * hi + (r % 4);
+          if (key >= N || (CAUSAL && key > qrow)) s[kt][r] = -INFINITY;
         }
       }
     }
 
-    // this wave's loads of the next block are in LDS; after the barrier every
-    // wave's are, and every wave is done reading this buffer
+    // block row maximum: 32 values in-lane, then the other lane half
+    float mx = fmaxf(s[0][0], s[1][0]);
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s[0][r], s[1][r]));
+    const float m_blk = max_across_halves(mx) * p.c;
+
+    const bool need = m_blk > m_run + kTau;
+    if (__any(need)) {
+      const float m_new = need ? m_blk : m_run;
+      const float alpha = need ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
+#pragma unroll
+      for (int mt = 0; mt < NMT; ++mt) oacc[mt] *= alpha;
+      l_run *= alpha;
+      m_run = m_new;
+    }
+    const float mu = (m_run == -INFINITY) ? 0.f : m_run;
+
+    // Straight-line region, written as 16 chunks that each compute one 16-bit
+    // pair of P for block j (two FMAs, two exponentials, the row-sum adds, one
+    // pack) and issue the next MFMA of GEMM-I for block j+1 (every chunk at
+    // d = 128, every other chunk at d = 64), so the matrix core and the VALU
+    // work side by side.  Operand reads are software-prefetched AHEAD MFMAs
+    // early from a small register ring; a scheduling fence after each chunk
+    // keeps the order and the live ranges.
+    constexpr int AHEAD = 4;
+    constexpr int NG1 = 2 * NKS;        // GEMM-I MFMAs per block
+    constexpr int STRIDE = 16 / NG1;    // chunks per GEMM-I MFMA
+    u32x4 kring[AHEAD];
+    s_next[0] = f32x16{};
+    s_next[1] = f32x16{};
+#pragma unroll
+    for (int m = 0; m < AHEAD; ++m) kring[m] = k_read(kb_next, m % 2, m / 2);
+    u32x4 pb[4];
+    float lsum = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      if (i % STRIDE == 0) {
+        const int m = i / STRIDE;       // MFMA m: k-step m / 2, key tile m % 2
+        const u32x4 a = kring[m % AHEAD];
+        if (m + AHEAD < NG1) kring[m % AHEAD] = k_read(kb_next, (m + AHEAD) % 2, (m + AHEAD) / 2);
+        s_next[m % 2] = Half<DT>::mfma(a, qf[m / 2], s_next[m % 2]);
+      }
+      // probabilities -> 16-bit P^T operands; the row sum stays in fp32 (a
+      // sum of the rounded values would carry their rounding into lse
+      // whenever a few keys dominate the row)
+      const int u = i / 4, w = i % 4;
+      const int r0 = 8 * (u % 2) + 2 * w;
+      const float e0 = __builtin_amdgcn_exp2f(fmaf(s[u / 2][r0], p.c, -mu));
+      const float e1 = __builtin_amdgcn_exp2f(fmaf(s[u / 2][r0 + 1], p.c, -mu));
+      pb[u][w] = Half<DT>::pack(e0, e1);
+      lsum += e0 + e1;
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    l_run += lsum;
+
+    // GEMM-II: O^T += V^T P^T, V^T gathered by transposing LDS reads, the
+    // reads running AHEAD MFMAs early
+    auto v_frag = [&](int t) {
+      const int mt = t / 4, u = t % 4;
+      const u32x2 a0 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 0));
+      const u32x2 a1 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 1));
+      return u32x4{a0[0], a0[1], a1[0], a1[1]};
+    };
+    constexpr int NV = 4 * NMT;
+    u32x4 vring[AHEAD];
+#pragma unroll
+    for (int t = 0; t < AHEAD; ++t) vring[t] = v_frag(t);
+#pragma unroll
+    for (int t = 0; t < NV; ++t) {
+      const u32x4 a = vring[t % AHEAD];
+      if (t + AHEAD < NV) vring[t % AHEAD] = v_frag(t + AHEAD);
+      oacc[t / 4] = Half<DT>::mfma(a, pb[t % 4], oacc[t / 4]);
+    }
+  };
+
+  // Pipeline, iteration j (P = j % 2): K(j+1) is in K buffer 1-P, V(j) in V
+  // buffer P, the scores of block j are in registers.  Issue the loads of
+  // K(j+2) into K buffer P (last read by GEMM-I of block j, an iteration ago)
+  // and V(j+1) into V buffer 1-P (last read by GEMM-II of block j-1); run
+  // GEMM-I of block j+1 alongside the softmax of block j; GEMM-II of block j.
+  // One barrier per iteration publishes the loads and retires the reads.
+  // Blocks a wave skips (causal) come only after all the blocks it computes.
+  f32x16 sa[2], sb[2];
+  auto iteration = [&](auto parity, int j, f32x16 (&s_cur)[2], f32x16 (&s_next)[2]) {
+    constexpr int P = decltype(parity)::value;
+    if (j + 2 < nkv) load_k((j + 2) * kBN, P);
+    if (j + 1 < nkv) load_v((j + 1) * kBN, 1 - P);
+    if (active(j)) block(j, 1 - P, P, s_cur, s_next);
     __builtin_amdgcn_s_waitcnt(kWaitLoads);
     __syncthreads();
   };
 
-  load_block(0, 0);
+  load_k(0, 0);
+  load_v(0, 0);
+  if (nkv > 1) load_k(kBN, 1);
   __builtin_amdgcn_s_waitcnt(kWaitLoads);
   __syncthreads();
+  if (active(0)) gemm1(0, sa);
+  __syncthreads();   // K buffer 0 is refilled in the first iteration
 
   for (int j = 0; j < nkv; j += 2) {
-    step(std::integral_constant<int, 0>{}, j);
-    if (j + 1 < nkv) step(std::integral_constant<int, 1>{}, j + 1);
+    iteration(std::integral_constant<int, 0>{}, j, sa, sb);
+    if (j + 1 < nkv) iteration(std::integral_constant<int, 1>{}, j + 1, sb, sa);
   }
 
   // ---- epilogue: O = O / l in the storage type, lse in natural log ----
@@ -386,7 +441,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
 
 template <int D>
 constexpr size_t lds_bytes() {
-  return 2 * (size_t)Layout<D>::BUF;
+  return 2 * (size_t)(Layout<D>::KBYTES + Layout<D>::VBYTES);
 }
 
 template <int D, int DT, bool CAUSAL>
