@@ -4,9 +4,10 @@
 //
 // Work decomposition (the paper's Method section gives each thread block a
 // fixed batch and head of Q, a (BM, HeadDim) tile at coordinate L = block
-// index): one workgroup owns BM = 128 query rows of one (batch, head); its four
-// wavefronts own 32 rows each and walk the key/value sequence in blocks of
-// BN = 64 keys (the loop of the paper's Appendix B listings).
+// index): one workgroup owns BM = 256 query rows of one (batch, head); its
+// eight wavefronts (two per SIMD) own 32 rows each and walk the key/value
+// sequence in blocks of BN = 64 keys (the loop of the paper's Appendix B
+// listings).  A K/V block staged in LDS serves all 256 rows.
 //
 // The two products use the 32x32x16 MFMA of CDNA4:
 //
@@ -14,8 +15,8 @@
 //            A operand = K rows read from LDS (K keeps its stored layout, the
 //            point of the paper's "GEMM error" case), B operand = Q, loaded
 //            once and resident in VGPRs.  The accumulator gives each lane one
-//            query column, so a query's row max / row sum is an in-register
-//            reduction plus one swap between the two lane halves sharing the
+//            query column, so a query's row statistics are in-register
+//            reductions plus one swap between the two lane halves sharing the
 //            column (v_permlane32_swap).
 //
 //   GEMM-II  O^T[d][query] += V^T[d][key] . P^T[key][query]
@@ -29,21 +30,20 @@
 //            pointing its four lane quads at exactly those four key rows.  The
 //            contraction order over keys is free, so nothing else changes.
 //
-// K/V staging: each key block goes HBM -> LDS with direct buffer loads
-// (buffer_load_dwordx4 ... lds; lane l's 16 bytes land at M0 + 16 l), issued
-// one block ahead into the other of two LDS buffers; one barrier per block.
-// Rows past the end of the sequence read as zeros (buffer range checking), so
-// no load needs a branch.  16-byte units are XOR-swizzled per row so that the
-// 128-bit K reads (16 rows, one column of units) and the transposing V reads
-// (4 rows x 4 units) each hit 16 distinct bank groups.
+// Pipeline: K and V blocks go HBM -> LDS with direct buffer loads
+// (buffer_load_dwordx4 ... lds; rows past the end of the sequence read as
+// zeros), K one block further ahead than V.  While the exponentials of block
+// j are formed, the MFMAs of GEMM-I for block j+1 run beside them (16
+// interleaved chunks); then GEMM-II of block j.  One barrier per block.
 //
-// Online softmax (exp2 domain, c = |scale| * log2 e):
-//   m_blk = c * max_j s_j;   p_j = 2^(c*s_j - m);   l += sum_j p_j (fp32)
-//   The running maximum m is only raised when a block's maximum exceeds it by
-//   more than TAU = 8 (then O and l are rescaled by 2^(m_old - m_new)).  The
-//   result is exact for any m not below the true maximum minus TAU: every p_j
-//   stays <= 2^8, and O = sum p v / sum p, lse = (m + log2 l) * ln 2 use the
-//   same m.  Rescaling becomes rare after the first blocks.
+// Online softmax (exp2 domain, c = |scale| * log2 e): probabilities
+// p = 2^(c s - m) are formed against the running maximum m without first
+// reducing the block's own maximum.  A lane whose 32 probabilities sum to at
+// most 2^8 has every p <= 2^8; only when some lane exceeds that (the running
+// maximum must rise; always on the first block) is the block's exact maximum
+// taken, O and l rescaled by 2^(m_old - m_new) and the probabilities redone.
+// O = sum p v / sum p and lse = (m + log2 l) ln 2 use the same m, so the
+// result is exact in either case.
 //
 // Causal masking: key blocks entirely above the diagonal of the workgroup are
 // never loaded; a wavefront skips the blocks entirely above its own rows;
@@ -55,6 +55,7 @@
 // share its L2 for the K/V stream.
 
 #include <hip/hip_runtime.h>
+#include <float.h>
 #include <math.h>
 #include <stdint.h>
 
@@ -78,11 +79,13 @@ typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 
-constexpr int kBM = 128;      // query rows per workgroup
+constexpr int kBM = 256;      // query rows per workgroup
 constexpr int kBN = 64;       // keys per block
-constexpr int kWaves = 4;     // 32 query rows per wavefront
+constexpr int kWaves = 8;     // 32 query rows per wavefront
 constexpr int kThreads = 64 * kWaves;
-constexpr float kTau = 8.0f;  // lazy-rescale threshold (log2 units)
+// Largest probability allowed against a stale running maximum, 2^8: sums of
+// 64K such values stay far from fp32 overflow and P fits fp16.
+constexpr float kPmax = 256.0f;
 constexpr int kXcds = 8;
 constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data
 // s_waitcnt immediate for vmcnt(0) and lgkmcnt(0): the direct LDS loads of
@@ -186,7 +189,7 @@ __device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t rs, void* lds,
 }
 
 template <int D, int DT, bool CAUSAL>
-__global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
+__global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
   using L = Layout<D>;
   constexpr int NKS = D / 16;          // GEMM-I k-steps
   constexpr int NMT = D / 32;          // GEMM-II M tiles
@@ -299,8 +302,34 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
   // for block j+1; then GEMM-II of block j.  GEMM-I always runs: on a wave's
   // last block it reads a stale (in-bounds) K buffer and its result is dropped,
   // which keeps a single code path and the register allocation compact.
+  // row maximum of a block's (masked) scores, both lane halves, raw units
+  auto row_max = [&](const f32x16 (&sc)[2]) __attribute__((always_inline)) {
+    float mx = fmaxf(sc[0][0], sc[1][0]);
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(sc[0][r], sc[1][r]));
+    return max_across_halves(mx);
+  };
+
+  // Block j.  Probabilities are formed against the running maximum m_run
+  // without looking at the block's own maximum; since every p >= 0, a lane
+  // whose 32 probabilities sum to at most 2^TAU has every p <= 2^TAU, which
+  // keeps all sums in range.  Only when some lane exceeds that (the running
+  // maximum must rise, and always on a wave's first block, where m_run is
+  // -inf) is the block's exact maximum taken, O and l rescaled and the
+  // probabilities recomputed.  Results are exact either way: O and lse use
+  // the same m_run.
   auto block = [&](int j, int kb_next, int vb, f32x16 (&s)[2], f32x16 (&s_next)[2]) {
     const int j0 = j * kBN;
+    constexpr int AHEAD = 4;
+    constexpr int NG1 = 2 * NKS;        // GEMM-I MFMAs per block
+    constexpr int STRIDE = 16 / NG1;    // exponential chunks per GEMM-I MFMA
+    constexpr int NV = 4 * NMT;         // GEMM-II MFMAs per block
+    // first K fragments of GEMM-I for block j+1: their LDS latency runs under
+    // the mask work below
+    u32x4 kring[AHEAD];
+#pragma unroll
+    for (int m = 0; m < AHEAD; ++m) kring[m] = k_read(kb_next, m % 2, m / 2);
+
     // mask: keys past the end of the sequence, keys after the query (causal)
     const bool need_mask = (j0 + kBN > N) || (CAUSAL && j0 + kBN - 1 > qw);
     if (need_mask) {
@@ -313,41 +342,43 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
         }
       }
     }
+    // before the first block m_run is -inf: offset by -FLT_MAX instead, so
+    // every visible key overflows to +inf and forces the exact path below
+    float mu = (m_run == -INFINITY) ? -FLT_MAX : m_run;
 
-    // block row maximum: 32 values in-lane, then the other lane half
-    float mx = fmaxf(s[0][0], s[1][0]);
-#pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s[0][r], s[1][r]));
-    const float m_blk = max_across_halves(mx) * p.c;
+    // GEMM-II operand: V^T fragment t (M tile t % NMT, key step t / NMT), so
+    // consecutive MFMAs accumulate into different O tiles
+    auto v_frag = [&](int t) __attribute__((always_inline)) {
+      const int mt = t % NMT, u = t / NMT;
+      const u32x2 a0 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 0));
+      const u32x2 a1 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 1));
+      return u32x4{a0[0], a0[1], a1[0], a1[1]};
+    };
 
-    const bool need = m_blk > m_run + kTau;
-    if (__any(need)) {
-      const float m_new = need ? m_blk : m_run;
-      const float alpha = need ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
-#pragma unroll
-      for (int mt = 0; mt < NMT; ++mt) oacc[mt] *= alpha;
-      l_run *= alpha;
-      m_run = m_new;
-    }
-    const float mu = (m_run == -INFINITY) ? 0.f : m_run;
-
-    // Straight-line region, written as 16 chunks that each compute one 16-bit
-    // pair of P for block j (two FMAs, two exponentials, the row-sum adds, one
-    // pack) and issue the next MFMA of GEMM-I for block j+1 (every chunk at
-    // d = 128, every other chunk at d = 64), so the matrix core and the VALU
-    // work side by side.  Operand reads are software-prefetched AHEAD MFMAs
-    // early from a small register ring; a scheduling fence after each chunk
-    // keeps the order and the live ranges.
-    constexpr int AHEAD = 4;
-    constexpr int NG1 = 2 * NKS;        // GEMM-I MFMAs per block
-    constexpr int STRIDE = 16 / NG1;    // chunks per GEMM-I MFMA
-    u32x4 kring[AHEAD];
-    s_next[0] = f32x16{};
-    s_next[1] = f32x16{};
-#pragma unroll
-    for (int m = 0; m < AHEAD; ++m) kring[m] = k_read(kb_next, m % 2, m / 2);
     u32x4 pb[4];
     float lsum = 0.f;
+    // one 16-bit pair of P^T (chunk i of 16): two FMAs, two exponentials, the
+    // row-sum adds, one pack.  The row sum stays in fp32 (a sum of the
+    // rounded values would carry their rounding into lse whenever a few keys
+    // dominate the row).
+    auto exp_chunk = [&](int i) __attribute__((always_inline)) {
+      const int u = i / 4, w = i % 4;
+      const int r0 = 8 * (u % 2) + 2 * w;
+      const float e0 = __builtin_amdgcn_exp2f(fmaf(s[u / 2][r0], p.c, -mu));
+      const float e1 = __builtin_amdgcn_exp2f(fmaf(s[u / 2][r0 + 1], p.c, -mu));
+      pb[u][w] = Half<DT>::pack(e0, e1);
+      lsum += e0 + e1;
+    };
+
+    // Straight-line region 1, written as 16 chunks that each compute one pair
+    // of P for block j and issue the next MFMA of GEMM-I for block j+1 (every
+    // chunk at d = 128, every other chunk at d = 64), so the matrix core and
+    // the VALU work side by side.  Operand reads run AHEAD MFMAs early from
+    // small register rings (the last chunks start on GEMM-II's V fragments);
+    // a scheduling fence after each chunk keeps the order and the live ranges.
+    s_next[0] = f32x16{};
+    s_next[1] = f32x16{};
+    u32x4 vring[AHEAD];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       if (i % STRIDE == 0) {
@@ -356,36 +387,34 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(KParams p) {
         if (m + AHEAD < NG1) kring[m % AHEAD] = k_read(kb_next, (m + AHEAD) % 2, (m + AHEAD) / 2);
         s_next[m % 2] = Half<DT>::mfma(a, qf[m / 2], s_next[m % 2]);
       }
-      // probabilities -> 16-bit P^T operands; the row sum stays in fp32 (a
-      // sum of the rounded values would carry their rounding into lse
-      // whenever a few keys dominate the row)
-      const int u = i / 4, w = i % 4;
-      const int r0 = 8 * (u % 2) + 2 * w;
-      const float e0 = __builtin_amdgcn_exp2f(fmaf(s[u / 2][r0], p.c, -mu));
-      const float e1 = __builtin_amdgcn_exp2f(fmaf(s[u / 2][r0 + 1], p.c, -mu));
-      pb[u][w] = Half<DT>::pack(e0, e1);
-      lsum += e0 + e1;
+      if (i >= 16 - AHEAD) vring[i - (16 - AHEAD)] = v_frag(i - (16 - AHEAD));
+      exp_chunk(i);
       __builtin_amdgcn_sched_barrier(0);
+    }
+
+    // exact path (rare): the running maximum rises
+    if (__any(lsum > kPmax)) {
+      const float m_blk = row_max(s) * p.c;
+      const float m_new = fmaxf(m_run, m_blk);
+      const float alpha = (m_run == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+#pragma unroll
+      for (int mt = 0; mt < NMT; ++mt) oacc[mt] *= alpha;
+      l_run *= alpha;
+      m_run = m_new;
+      mu = (m_run == -INFINITY) ? 0.f : m_run;
+      lsum = 0.f;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) exp_chunk(i);
     }
     l_run += lsum;
 
-    // GEMM-II: O^T += V^T P^T, V^T gathered by transposing LDS reads, the
-    // reads running AHEAD MFMAs early
-    auto v_frag = [&](int t) {
-      const int mt = t / 4, u = t % 4;
-      const u32x2 a0 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 0));
-      const u32x2 a1 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 1));
-      return u32x4{a0[0], a0[1], a1[0], a1[1]};
-    };
-    constexpr int NV = 4 * NMT;
-    u32x4 vring[AHEAD];
-#pragma unroll
-    for (int t = 0; t < AHEAD; ++t) vring[t] = v_frag(t);
+    // Straight-line region 2: GEMM-II, O^T += V^T P^T
 #pragma unroll
     for (int t = 0; t < NV; ++t) {
       const u32x4 a = vring[t % AHEAD];
       if (t + AHEAD < NV) vring[t % AHEAD] = v_frag(t + AHEAD);
-      oacc[t / 4] = Half<DT>::mfma(a, pb[t % 4], oacc[t / 4]);
+      oacc[t % NMT] = Half<DT>::mfma(a, pb[t / NMT], oacc[t % NMT]);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
