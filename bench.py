@@ -39,6 +39,7 @@ import seeded_inputs as si  # noqa: E402
 
 METRIC = "attention fwd TFLOPS (4·B·H·N²·d, ½ if causal) and % of MFMA peak"
 PEAK_TFLOPS = 2500.0          # MI355X dense bf16/fp16 MFMA, published
+PEAK_FLOP_PER_CLK = 256 * 4096  # 256 CUs x 4096 dense bf16 flop per clock
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2506_12355_amd", "csrc", "attn_fwd_gfx950.hip")
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_fwd_bf16_d128_n8192_hbm_traffic.md")
 
@@ -63,6 +64,55 @@ def committed_traffic():
     if not sha or not val or sha.group(1) != kernel_source_sha256():
         return None
     return float(val.group(1))
+
+
+# --------------------------------------------------------------------------
+# shader clock during the timed region (rocm-smi, sampled from a thread)
+# --------------------------------------------------------------------------
+class SclkSampler:
+    """Samples the current SCLK with rocm-smi while the timed steps run."""
+
+    def __init__(self, period_s=0.2):
+        import threading
+        self.period_s = period_s
+        self.samples = []
+        self._stop = threading.Event()
+        self._thread = threading.Thread(target=self._run, daemon=True)
+
+    def _read(self):
+        import subprocess
+        out = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True,
+                             text=True, timeout=10).stdout
+        data = json.loads(out)
+        for card in data.values():
+            m = re.search(r"(\d+)\s*Mhz", str(card.get("sclk clock speed:", "")))
+            if m:
+                return int(m.group(1))
+        return None
+
+    def _run(self):
+        while not self._stop.is_set():
+            try:
+                v = self._read()
+                if v:
+                    self.samples.append(v)
+            except Exception:
+                pass
+            self._stop.wait(self.period_s)
+
+    def __enter__(self):
+        self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        self._thread.join(timeout=15)
+
+    def median(self):
+        if not self.samples:
+            return None
+        v = sorted(self.samples)
+        return v[len(v) // 2]
 
 
 # --------------------------------------------------------------------------
@@ -106,8 +156,8 @@ def cpu_baseline(w, q, k, v, max_workers=16):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the CPU oracle leg (for profiler runs)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -162,11 +212,12 @@ def main():
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)]
               for _ in range(args.steps)]
     torch.cuda.synchronize(dev)
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(events[i])
-    torch.cuda.synchronize(dev)
-    wall = time.perf_counter() - t0
+    with SclkSampler() as sclk:
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            step(events[i])
+        torch.cuda.synchronize(dev)
+        wall = time.perf_counter() - t0
 
     nc_ms = [e[0].elapsed_time(e[1]) for e in events]
     c_ms = [e[1].elapsed_time(e[2]) for e in events]
@@ -204,6 +255,9 @@ def main():
             "masks": ["none", "causal"], "seed": w.seed,
         },
         "pct_of_peak": round(100.0 * value / PEAK_TFLOPS, 2),
+        "sclk_mhz": sclk.median(),
+        "pct_of_peak_at_sclk": (round(100.0 * value / (PEAK_FLOP_PER_CLK * sclk.median() * 1e6 / 1e12), 2)
+                                if sclk.median() else None),
         "per_launch": {
             "unmasked": {"ms": round(nc_mean, 4), "tflops": round(achieved, 2)},
             "causal": {"ms": round(c_mean, 4),
