@@ -34,7 +34,8 @@
 // (buffer_load_dwordx4 ... lds; rows past the end of the sequence read as
 // zeros), K one block further ahead than V.  While the exponentials of block
 // j are formed, the MFMAs of GEMM-I for block j+1 run beside them (16
-// interleaved chunks); then GEMM-II of block j.  One barrier per block.
+// interleaved slots, the exponentials software-pipelined three deep, the wave
+// at raised issue priority); then GEMM-II of block j.  One barrier per block.
 //
 // Online softmax (exp2 domain, c = |scale| * log2 e): probabilities
 // p = 2^(c s - m) are formed against the running maximum m without first
@@ -370,15 +371,33 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
       lsum += e0 + e1;
     };
 
-    // Straight-line region 1, written as 16 chunks that each compute one pair
-    // of P for block j and issue the next MFMA of GEMM-I for block j+1 (every
-    // chunk at d = 128, every other chunk at d = 64), so the matrix core and
-    // the VALU work side by side.  Operand reads run AHEAD MFMAs early from
-    // small register rings (the last chunks start on GEMM-II's V fragments);
-    // a scheduling fence after each chunk keeps the order and the live ranges.
+    // Straight-line region 1, written as 16 slots that each issue the next
+    // MFMA of GEMM-I for block j+1 (every slot at d = 128, every other slot at
+    // d = 64) and advance the exponentials of block j through a three-stage
+    // software pipeline: the FMAs of pair i+2, the exponentials of pair i+1,
+    // and the pack and row-sum adds of pair i, so that no instruction waits
+    // on a result produced in its own slot.  Operand reads run AHEAD MFMAs
+    // early from small register rings (the last slots start on GEMM-II's V
+    // fragments); a scheduling fence after each slot keeps the order and the
+    // live ranges.
     s_next[0] = f32x16{};
     s_next[1] = f32x16{};
     u32x4 vring[AHEAD];
+    float xa[18], xb[18], ea[17], eb[17];
+    float lsum_even = 0.f, lsum_odd = 0.f;
+    auto arg = [&](int i, int k) __attribute__((always_inline)) {
+      const int u = i / 4, w = i % 4;
+      return fmaf(s[u / 2][8 * (u % 2) + 2 * w + k], p.c, -mu);
+    };
+    // Raised issue priority while this wave has both MFMAs and VALU work: the
+    // other wave of the SIMD, in its MFMA-only GEMM-II, fills the gaps.
+    __builtin_amdgcn_s_setprio(1);
+    xa[0] = arg(0, 0);
+    xb[0] = arg(0, 1);
+    xa[1] = arg(1, 0);
+    xb[1] = arg(1, 1);
+    ea[0] = __builtin_amdgcn_exp2f(xa[0]);
+    eb[0] = __builtin_amdgcn_exp2f(xb[0]);
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       if (i % STRIDE == 0) {
@@ -388,9 +407,24 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
         s_next[m % 2] = Half<DT>::mfma(a, qf[m / 2], s_next[m % 2]);
       }
       if (i >= 16 - AHEAD) vring[i - (16 - AHEAD)] = v_frag(i - (16 - AHEAD));
-      exp_chunk(i);
+      if (i + 1 < 16) {
+        ea[i + 1] = __builtin_amdgcn_exp2f(xa[i + 1]);
+        eb[i + 1] = __builtin_amdgcn_exp2f(xb[i + 1]);
+      }
+      if (i + 2 < 16) {
+        xa[i + 2] = arg(i + 2, 0);
+        xb[i + 2] = arg(i + 2, 1);
+      }
+      // 16-bit P^T operands; the row sum stays in fp32 (a sum of the rounded
+      // values would carry their rounding into lse whenever a few keys
+      // dominate the row)
+      pb[i / 4][i % 4] = Half<DT>::pack(ea[i], eb[i]);
+      if (i % 2 == 0) lsum_even += ea[i] + eb[i];
+      else lsum_odd += ea[i] + eb[i];
       __builtin_amdgcn_sched_barrier(0);
     }
+    __builtin_amdgcn_s_setprio(0);
+    lsum = lsum_even + lsum_odd;
 
     // exact path (rare): the running maximum rises
     if (__any(lsum > kPmax)) {
