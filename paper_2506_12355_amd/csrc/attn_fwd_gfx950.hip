@@ -100,8 +100,9 @@ struct KParams {
   uint16_t* o;
   float* lse;
   int N;
-  int nq;      // query blocks per head
-  int total;   // nq * B * H workgroups
+  int nq;           // query blocks per head
+  int wg_per_head;  // workgroups per head: nq, or ceil(nq / 2) pairs when causal
+  int total;        // wg_per_head * B * H workgroups
   float c;     // |scale| * log2 e
   int qmode;
 };
@@ -205,13 +206,20 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
   const int hi = lane >> 5;
   const int N = p.N;
 
-  // ---- which (batch*head, query block) this workgroup owns ----
+  // ---- which (batch*head) and query block(s) this workgroup owns ----
+  // Unmasked: one query block.  Causal: query block qb costs qb + 1 units of
+  // key blocks, so a workgroup takes the pair (nq-1-i, i), the longer first:
+  // every pair costs the same and the grid has no long tail.
   int id = blockIdx.x;
   const int per_xcd = p.total / kXcds;
   if (id < per_xcd * kXcds) id = (id % kXcds) * per_xcd + id / kXcds;
-  const int bh = id / p.nq;
-  int qb = id - bh * p.nq;
-  if (CAUSAL) qb = p.nq - 1 - qb;  // longest rows first
+  const int bh = id / p.wg_per_head;
+  const int slot_in_head = id - bh * p.wg_per_head;
+  int qbs[2] = {slot_in_head, -1};
+  if (CAUSAL) {
+    qbs[0] = p.nq - 1 - slot_in_head;
+    qbs[1] = (slot_in_head != p.nq - 1 - slot_in_head) ? slot_in_head : -1;
+  }
 
   const size_t head = (size_t)bh * (size_t)N * D;
   const uint32_t head_bytes = (uint32_t)N * D * 2;
@@ -219,287 +227,291 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(p.k + head, head_bytes);
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(p.v + head, head_bytes);
 
-  const int q0 = qb * kBM;
-  const int qw = q0 + wave * 32;   // first query row of this wavefront
-  const int qrow = qw + l32;       // the query row whose column this lane holds
+  auto run = [&](int qb) __attribute__((always_inline)) {
+    const int q0 = qb * kBM;
+    const int qw = q0 + wave * 32;   // first query row of this wavefront
+    const int qrow = qw + l32;       // the query row whose column this lane holds
 
-  // ---- Q: B operand of GEMM-I, resident for the whole key loop ----
-  u32x4 qf[NKS];
-#pragma unroll
-  for (int ks = 0; ks < NKS; ++ks) {
-    qf[ks] = __builtin_amdgcn_raw_buffer_load_b128(rq, (uint32_t)(qrow * D + 16 * ks + 8 * hi) * 2, 0, 0);
-    if (p.qmode == kQNegate) qf[ks] ^= 0x80008000u;
-    if (p.qmode == kQZero) qf[ks] = u32x4{0, 0, 0, 0};
-  }
-
-  const int kv_end = CAUSAL ? min(N, q0 + kBM) : N;
-  const int nkv = (kv_end + kBN - 1) / kBN;
-
-  f32x16 oacc[NMT];
-#pragma unroll
-  for (int mt = 0; mt < NMT; ++mt) oacc[mt] = f32x16{};
-  float m_run = -INFINITY;   // running maximum, exp2 domain
-  float l_run = 0.f;         // this lane's share of the running row sum
-
-  // ---- HBM -> LDS: this wave's load groups of one K or V block ----
-  // LDS: K buffers 0 and 1, then V buffers 0 and 1
-  constexpr int VOFF = 2 * L::KBYTES;
-  // lane part of the global offset (row slot, 16-byte unit); the rest is uniform
-  const uint32_t load_lane_off = (uint32_t)(L::NG * (lane / L::U) * D * 2 + (lane % L::U) * 16);
-  auto load_k = [&](int j0, int kb) {
-#pragma unroll
-    for (int i = 0; i < GPW; ++i) {
-      const int g = wave * GPW + i;
-      lds_load16(rk, lds + kb * L::KBYTES + g * L::KGS, load_lane_off, (uint32_t)((j0 + g) * D) * 2);
-    }
-  };
-  auto load_v = [&](int j0, int vb) {
-#pragma unroll
-    for (int i = 0; i < GPW; ++i) {
-      const int g = wave * GPW + i;
-      lds_load16(rv, lds + VOFF + vb * L::VBYTES + g * L::VGS, load_lane_off,
-                 (uint32_t)((j0 + g) * D) * 2);
-    }
-  };
-
-  // per-lane LDS byte bases of the operand reads; every read adds a constant
-  //   K (A of GEMM-I): row r = 32 kt + l32 -> group r % NG, slot r / NG; unit 2 ks + hi
-  const int k_base = (l32 % L::NG) * L::KGS + (l32 / L::NG) * L::ROW + 16 * hi;
-  //   V (A of GEMM-II, transposing read): key = 16 u + 8 h2 + kq, dims d0 .. d0+3
-  const int grp = lane >> 4;
-  const int sl = lane & 15;
-  const int kq = 4 * (grp >> 1) + (sl >> 2);
-  const int v_base = VOFF + kq * L::VGS + 2 * (16 * (grp & 1) + 4 * (sl & 3));
-
-  auto k_read = [&](int kb, int kt, int ks) {
-    constexpr int SLOTS_PER_32 = 32 / L::NG;
-    return *reinterpret_cast<const u32x4*>(lds + kb * L::KBYTES + k_base +
-                                           kt * SLOTS_PER_32 * L::ROW + 32 * ks);
-  };
-  auto v_read = [&](int vb, int mt, int u, int h2) {
-    // group of key 16 u + 8 h2 + kq is (16 u + 8 h2) % NG + kq, slot (16 u + 8 h2) / NG
-    const int g_off = (16 * u + 8 * h2) % L::NG;
-    const int slot = (16 * u + 8 * h2) / L::NG;
-    return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_i16x4*)(lds + vb * L::VBYTES + v_base + g_off * L::VGS + slot * L::ROW + 64 * mt));
-  };
-
-  // whether this wave has a visible key in block j (causal: blocks above its rows are skipped)
-  auto active = [&](int j) { return (qw < N) && (!CAUSAL || j * kBN <= qw + 31); };
-
-  // GEMM-I: two 32-key tiles of S^T for the block in K buffer kb
-  auto gemm1 = [&](int kb, f32x16 (&s)[2]) {
-    s[0] = f32x16{};
-    s[1] = f32x16{};
-#pragma unroll
+    // ---- Q: B operand of GEMM-I, resident for the whole key loop ----
+    u32x4 qf[NKS];
+  #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) s[kt] = Half<DT>::mfma(k_read(kb, kt, ks), qf[ks], s[kt]);
+      qf[ks] = __builtin_amdgcn_raw_buffer_load_b128(rq, (uint32_t)(qrow * D + 16 * ks + 8 * hi) * 2, 0, 0);
+      if (p.qmode == kQNegate) qf[ks] ^= 0x80008000u;
+      if (p.qmode == kQZero) qf[ks] = u32x4{0, 0, 0, 0};
     }
-  };
 
-  // Block j: mask, row max and (rare) rescale; then, in one straight-line
-  // region, the exponentials of block j interleaved with the MFMAs of GEMM-I
-  // for block j+1; then GEMM-II of block j.  GEMM-I always runs: on a wave's
-  // last block it reads a stale (in-bounds) K buffer and its result is dropped,
-  // which keeps a single code path and the register allocation compact.
-  // row maximum of a block's (masked) scores, both lane halves, raw units
-  auto row_max = [&](const f32x16 (&sc)[2]) __attribute__((always_inline)) {
-    float mx = fmaxf(sc[0][0], sc[1][0]);
-#pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(sc[0][r], sc[1][r]));
-    return max_across_halves(mx);
-  };
+    const int kv_end = CAUSAL ? min(N, q0 + kBM) : N;
+    const int nkv = (kv_end + kBN - 1) / kBN;
 
-  // Block j.  Probabilities are formed against the running maximum m_run
-  // without looking at the block's own maximum; since every p >= 0, a lane
-  // whose 32 probabilities sum to at most 2^TAU has every p <= 2^TAU, which
-  // keeps all sums in range.  Only when some lane exceeds that (the running
-  // maximum must rise, and always on a wave's first block, where m_run is
-  // -inf) is the block's exact maximum taken, O and l rescaled and the
-  // probabilities recomputed.  Results are exact either way: O and lse use
-  // the same m_run.
-  auto block = [&](int j, int kb_next, int vb, f32x16 (&s)[2], f32x16 (&s_next)[2]) {
-    const int j0 = j * kBN;
-    constexpr int AHEAD = 4;
-    constexpr int NG1 = 2 * NKS;        // GEMM-I MFMAs per block
-    constexpr int STRIDE = 16 / NG1;    // exponential chunks per GEMM-I MFMA
-    constexpr int NV = 4 * NMT;         // GEMM-II MFMAs per block
-    // first K fragments of GEMM-I for block j+1: their LDS latency runs under
-    // the mask work below
-    u32x4 kring[AHEAD];
-#pragma unroll
-    for (int m = 0; m < AHEAD; ++m) kring[m] = k_read(kb_next, m % 2, m / 2);
+    f32x16 oacc[NMT];
+  #pragma unroll
+    for (int mt = 0; mt < NMT; ++mt) oacc[mt] = f32x16{};
+    float m_run = -INFINITY;   // running maximum, exp2 domain
+    float l_run = 0.f;         // this lane's share of the running row sum
 
-    // mask: keys past the end of the sequence, keys after the query (causal)
-    const bool need_mask = (j0 + kBN > N) || (CAUSAL && j0 + kBN - 1 > qw);
-    if (need_mask) {
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = j0 + 32 * kt + 8 * (r / 4) + 4 * hi + (r % 4);
-          if (key >= N || (CAUSAL && key > qrow)) s[kt][r] = -INFINITY;
+    // ---- HBM -> LDS: this wave's load groups of one K or V block ----
+    // LDS: K buffers 0 and 1, then V buffers 0 and 1
+    constexpr int VOFF = 2 * L::KBYTES;
+    // lane part of the global offset (row slot, 16-byte unit); the rest is uniform
+    const uint32_t load_lane_off = (uint32_t)(L::NG * (lane / L::U) * D * 2 + (lane % L::U) * 16);
+    auto load_k = [&](int j0, int kb) {
+  #pragma unroll
+      for (int i = 0; i < GPW; ++i) {
+        const int g = wave * GPW + i;
+        lds_load16(rk, lds + kb * L::KBYTES + g * L::KGS, load_lane_off, (uint32_t)((j0 + g) * D) * 2);
+      }
+    };
+    auto load_v = [&](int j0, int vb) {
+  #pragma unroll
+      for (int i = 0; i < GPW; ++i) {
+        const int g = wave * GPW + i;
+        lds_load16(rv, lds + VOFF + vb * L::VBYTES + g * L::VGS, load_lane_off,
+                   (uint32_t)((j0 + g) * D) * 2);
+      }
+    };
+
+    // per-lane LDS byte bases of the operand reads; every read adds a constant
+    //   K (A of GEMM-I): row r = 32 kt + l32 -> group r % NG, slot r / NG; unit 2 ks + hi
+    const int k_base = (l32 % L::NG) * L::KGS + (l32 / L::NG) * L::ROW + 16 * hi;
+    //   V (A of GEMM-II, transposing read): key = 16 u + 8 h2 + kq, dims d0 .. d0+3
+    const int grp = lane >> 4;
+    const int sl = lane & 15;
+    const int kq = 4 * (grp >> 1) + (sl >> 2);
+    const int v_base = VOFF + kq * L::VGS + 2 * (16 * (grp & 1) + 4 * (sl & 3));
+
+    auto k_read = [&](int kb, int kt, int ks) {
+      constexpr int SLOTS_PER_32 = 32 / L::NG;
+      return *reinterpret_cast<const u32x4*>(lds + kb * L::KBYTES + k_base +
+                                             kt * SLOTS_PER_32 * L::ROW + 32 * ks);
+    };
+    auto v_read = [&](int vb, int mt, int u, int h2) {
+      // group of key 16 u + 8 h2 + kq is (16 u + 8 h2) % NG + kq, slot (16 u + 8 h2) / NG
+      const int g_off = (16 * u + 8 * h2) % L::NG;
+      const int slot = (16 * u + 8 * h2) / L::NG;
+      return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (lds_i16x4*)(lds + vb * L::VBYTES + v_base + g_off * L::VGS + slot * L::ROW + 64 * mt));
+    };
+
+    // whether this wave has a visible key in block j (causal: blocks above its rows are skipped)
+    auto active = [&](int j) { return (qw < N) && (!CAUSAL || j * kBN <= qw + 31); };
+
+    // GEMM-I: two 32-key tiles of S^T for the block in K buffer kb
+    auto gemm1 = [&](int kb, f32x16 (&s)[2]) {
+      s[0] = f32x16{};
+      s[1] = f32x16{};
+  #pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) {
+  #pragma unroll
+        for (int kt = 0; kt < 2; ++kt) s[kt] = Half<DT>::mfma(k_read(kb, kt, ks), qf[ks], s[kt]);
+      }
+    };
+
+    // Block j: mask, row max and (rare) rescale; then, in one straight-line
+    // region, the exponentials of block j interleaved with the MFMAs of GEMM-I
+    // for block j+1; then GEMM-II of block j.  GEMM-I always runs: on a wave's
+    // last block it reads a stale (in-bounds) K buffer and its result is dropped,
+    // which keeps a single code path and the register allocation compact.
+    // row maximum of a block's (masked) scores, both lane halves, raw units
+    auto row_max = [&](const f32x16 (&sc)[2]) __attribute__((always_inline)) {
+      float mx = fmaxf(sc[0][0], sc[1][0]);
+  #pragma unroll
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(sc[0][r], sc[1][r]));
+      return max_across_halves(mx);
+    };
+
+    // Block j.  Probabilities are formed against the running maximum m_run
+    // without looking at the block's own maximum; since every p >= 0, a lane
+    // whose 32 probabilities sum to at most 2^TAU has every p <= 2^TAU, which
+    // keeps all sums in range.  Only when some lane exceeds that (the running
+    // maximum must rise, and always on a wave's first block, where m_run is
+    // -inf) is the block's exact maximum taken, O and l rescaled and the
+    // probabilities recomputed.  Results are exact either way: O and lse use
+    // the same m_run.
+    auto block = [&](int j, int kb_next, int vb, f32x16 (&s)[2], f32x16 (&s_next)[2]) {
+      const int j0 = j * kBN;
+      constexpr int AHEAD = 4;
+      constexpr int NG1 = 2 * NKS;        // GEMM-I MFMAs per block
+      constexpr int STRIDE = 16 / NG1;    // exponential chunks per GEMM-I MFMA
+      constexpr int NV = 4 * NMT;         // GEMM-II MFMAs per block
+      // first K fragments of GEMM-I for block j+1: their LDS latency runs under
+      // the mask work below
+      u32x4 kring[AHEAD];
+  #pragma unroll
+      for (int m = 0; m < AHEAD; ++m) kring[m] = k_read(kb_next, m % 2, m / 2);
+
+      // mask: keys past the end of the sequence, keys after the query (causal)
+      const bool need_mask = (j0 + kBN > N) || (CAUSAL && j0 + kBN - 1 > qw);
+      if (need_mask) {
+  #pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+  #pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = j0 + 32 * kt + 8 * (r / 4) + 4 * hi + (r % 4);
+            if (key >= N || (CAUSAL && key > qrow)) s[kt][r] = -INFINITY;
+          }
         }
       }
-    }
-    // before the first block m_run is -inf: offset by -FLT_MAX instead, so
-    // every visible key overflows to +inf and forces the exact path below
-    float mu = (m_run == -INFINITY) ? -FLT_MAX : m_run;
+      // before the first block m_run is -inf: offset by -FLT_MAX instead, so
+      // every visible key overflows to +inf and forces the exact path below
+      float mu = (m_run == -INFINITY) ? -FLT_MAX : m_run;
 
-    // GEMM-II operand: V^T fragment t (M tile t % NMT, key step t / NMT), so
-    // consecutive MFMAs accumulate into different O tiles
-    auto v_frag = [&](int t) __attribute__((always_inline)) {
-      const int mt = t % NMT, u = t / NMT;
-      const u32x2 a0 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 0));
-      const u32x2 a1 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 1));
-      return u32x4{a0[0], a0[1], a1[0], a1[1]};
+      // GEMM-II operand: V^T fragment t (M tile t % NMT, key step t / NMT), so
+      // consecutive MFMAs accumulate into different O tiles
+      auto v_frag = [&](int t) __attribute__((always_inline)) {
+        const int mt = t % NMT, u = t / NMT;
+        const u32x2 a0 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 0));
+        const u32x2 a1 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 1));
+        return u32x4{a0[0], a0[1], a1[0], a1[1]};
+      };
+
+      u32x4 pb[4];
+      float lsum = 0.f;
+      // one 16-bit pair of P^T (chunk i of 16): two FMAs, two exponentials, the
+      // row-sum adds, one pack.  The row sum stays in fp32 (a sum of the
+      // rounded values would carry their rounding into lse whenever a few keys
+      // dominate the row).
+      auto exp_chunk = [&](int i) __attribute__((always_inline)) {
+        const int u = i / 4, w = i % 4;
+        const int r0 = 8 * (u % 2) + 2 * w;
+        const float e0 = __builtin_amdgcn_exp2f(fmaf(s[u / 2][r0], p.c, -mu));
+        const float e1 = __builtin_amdgcn_exp2f(fmaf(s[u / 2][r0 + 1], p.c, -mu));
+        pb[u][w] = Half<DT>::pack(e0, e1);
+        lsum += e0 + e1;
+      };
+
+      // Straight-line region 1, written as 16 slots that each issue the next
+      // MFMA of GEMM-I for block j+1 (every slot at d = 128, every other slot at
+      // d = 64) and advance the exponentials of block j through a three-stage
+      // software pipeline: the FMAs of pair i+2, the exponentials of pair i+1,
+      // and the pack and row-sum adds of pair i, so that no instruction waits
+      // on a result produced in its own slot.  Operand reads run AHEAD MFMAs
+      // early from small register rings (the last slots start on GEMM-II's V
+      // fragments); a scheduling fence after each slot keeps the order and the
+      // live ranges.
+      s_next[0] = f32x16{};
+      s_next[1] = f32x16{};
+      u32x4 vring[AHEAD];
+      float xa[18], xb[18], ea[17], eb[17];
+      float lsum_even = 0.f, lsum_odd = 0.f;
+      auto arg = [&](int i, int k) __attribute__((always_inline)) {
+        const int u = i / 4, w = i % 4;
+        return fmaf(s[u / 2][8 * (u % 2) + 2 * w + k], p.c, -mu);
+      };
+      // Raised issue priority while this wave has both MFMAs and VALU work: the
+      // other wave of the SIMD, in its MFMA-only GEMM-II, fills the gaps.
+      __builtin_amdgcn_s_setprio(1);
+      xa[0] = arg(0, 0);
+      xb[0] = arg(0, 1);
+      xa[1] = arg(1, 0);
+      xb[1] = arg(1, 1);
+      ea[0] = __builtin_amdgcn_exp2f(xa[0]);
+      eb[0] = __builtin_amdgcn_exp2f(xb[0]);
+  #pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        if (i % STRIDE == 0) {
+          const int m = i / STRIDE;       // MFMA m: k-step m / 2, key tile m % 2
+          const u32x4 a = kring[m % AHEAD];
+          if (m + AHEAD < NG1) kring[m % AHEAD] = k_read(kb_next, (m + AHEAD) % 2, (m + AHEAD) / 2);
+          s_next[m % 2] = Half<DT>::mfma(a, qf[m / 2], s_next[m % 2]);
+        }
+        if (i >= 16 - AHEAD) vring[i - (16 - AHEAD)] = v_frag(i - (16 - AHEAD));
+        if (i + 1 < 16) {
+          ea[i + 1] = __builtin_amdgcn_exp2f(xa[i + 1]);
+          eb[i + 1] = __builtin_amdgcn_exp2f(xb[i + 1]);
+        }
+        if (i + 2 < 16) {
+          xa[i + 2] = arg(i + 2, 0);
+          xb[i + 2] = arg(i + 2, 1);
+        }
+        // 16-bit P^T operands; the row sum stays in fp32 (a sum of the rounded
+        // values would carry their rounding into lse whenever a few keys
+        // dominate the row)
+        pb[i / 4][i % 4] = Half<DT>::pack(ea[i], eb[i]);
+        if (i % 2 == 0) lsum_even += ea[i] + eb[i];
+        else lsum_odd += ea[i] + eb[i];
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      __builtin_amdgcn_s_setprio(0);
+      lsum = lsum_even + lsum_odd;
+
+      // exact path (rare): the running maximum rises
+      if (__any(lsum > kPmax)) {
+        const float m_blk = row_max(s) * p.c;
+        const float m_new = fmaxf(m_run, m_blk);
+        const float alpha = (m_run == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+  #pragma unroll
+        for (int mt = 0; mt < NMT; ++mt) oacc[mt] *= alpha;
+        l_run *= alpha;
+        m_run = m_new;
+        mu = (m_run == -INFINITY) ? 0.f : m_run;
+        lsum = 0.f;
+  #pragma unroll
+        for (int i = 0; i < 16; ++i) exp_chunk(i);
+      }
+      l_run += lsum;
+
+      // Straight-line region 2: GEMM-II, O^T += V^T P^T
+  #pragma unroll
+      for (int t = 0; t < NV; ++t) {
+        const u32x4 a = vring[t % AHEAD];
+        if (t + AHEAD < NV) vring[t % AHEAD] = v_frag(t + AHEAD);
+        oacc[t % NMT] = Half<DT>::mfma(a, pb[t / NMT], oacc[t % NMT]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     };
 
-    u32x4 pb[4];
-    float lsum = 0.f;
-    // one 16-bit pair of P^T (chunk i of 16): two FMAs, two exponentials, the
-    // row-sum adds, one pack.  The row sum stays in fp32 (a sum of the
-    // rounded values would carry their rounding into lse whenever a few keys
-    // dominate the row).
-    auto exp_chunk = [&](int i) __attribute__((always_inline)) {
-      const int u = i / 4, w = i % 4;
-      const int r0 = 8 * (u % 2) + 2 * w;
-      const float e0 = __builtin_amdgcn_exp2f(fmaf(s[u / 2][r0], p.c, -mu));
-      const float e1 = __builtin_amdgcn_exp2f(fmaf(s[u / 2][r0 + 1], p.c, -mu));
-      pb[u][w] = Half<DT>::pack(e0, e1);
-      lsum += e0 + e1;
+    // Pipeline, iteration j (P = j % 2): K(j+1) is in K buffer 1-P, V(j) in V
+    // buffer P, the scores of block j are in registers.  Issue the loads of
+    // K(j+2) into K buffer P (last read by GEMM-I of block j, an iteration ago)
+    // and V(j+1) into V buffer 1-P (last read by GEMM-II of block j-1); run
+    // GEMM-I of block j+1 alongside the softmax of block j; GEMM-II of block j.
+    // One barrier per iteration publishes the loads and retires the reads.
+    // Blocks a wave skips (causal) come only after all the blocks it computes.
+    f32x16 sa[2], sb[2];
+    auto iteration = [&](auto parity, int j, f32x16 (&s_cur)[2], f32x16 (&s_next)[2]) {
+      constexpr int P = decltype(parity)::value;
+      if (j + 2 < nkv) load_k((j + 2) * kBN, P);
+      if (j + 1 < nkv) load_v((j + 1) * kBN, 1 - P);
+      if (active(j)) block(j, 1 - P, P, s_cur, s_next);
+      __builtin_amdgcn_s_waitcnt(kWaitLoads);
+      __syncthreads();
     };
 
-    // Straight-line region 1, written as 16 slots that each issue the next
-    // MFMA of GEMM-I for block j+1 (every slot at d = 128, every other slot at
-    // d = 64) and advance the exponentials of block j through a three-stage
-    // software pipeline: the FMAs of pair i+2, the exponentials of pair i+1,
-    // and the pack and row-sum adds of pair i, so that no instruction waits
-    // on a result produced in its own slot.  Operand reads run AHEAD MFMAs
-    // early from small register rings (the last slots start on GEMM-II's V
-    // fragments); a scheduling fence after each slot keeps the order and the
-    // live ranges.
-    s_next[0] = f32x16{};
-    s_next[1] = f32x16{};
-    u32x4 vring[AHEAD];
-    float xa[18], xb[18], ea[17], eb[17];
-    float lsum_even = 0.f, lsum_odd = 0.f;
-    auto arg = [&](int i, int k) __attribute__((always_inline)) {
-      const int u = i / 4, w = i % 4;
-      return fmaf(s[u / 2][8 * (u % 2) + 2 * w + k], p.c, -mu);
-    };
-    // Raised issue priority while this wave has both MFMAs and VALU work: the
-    // other wave of the SIMD, in its MFMA-only GEMM-II, fills the gaps.
-    __builtin_amdgcn_s_setprio(1);
-    xa[0] = arg(0, 0);
-    xb[0] = arg(0, 1);
-    xa[1] = arg(1, 0);
-    xb[1] = arg(1, 1);
-    ea[0] = __builtin_amdgcn_exp2f(xa[0]);
-    eb[0] = __builtin_amdgcn_exp2f(xb[0]);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      if (i % STRIDE == 0) {
-        const int m = i / STRIDE;       // MFMA m: k-step m / 2, key tile m % 2
-        const u32x4 a = kring[m % AHEAD];
-        if (m + AHEAD < NG1) kring[m % AHEAD] = k_read(kb_next, (m + AHEAD) % 2, (m + AHEAD) / 2);
-        s_next[m % 2] = Half<DT>::mfma(a, qf[m / 2], s_next[m % 2]);
-      }
-      if (i >= 16 - AHEAD) vring[i - (16 - AHEAD)] = v_frag(i - (16 - AHEAD));
-      if (i + 1 < 16) {
-        ea[i + 1] = __builtin_amdgcn_exp2f(xa[i + 1]);
-        eb[i + 1] = __builtin_amdgcn_exp2f(xb[i + 1]);
-      }
-      if (i + 2 < 16) {
-        xa[i + 2] = arg(i + 2, 0);
-        xb[i + 2] = arg(i + 2, 1);
-      }
-      // 16-bit P^T operands; the row sum stays in fp32 (a sum of the rounded
-      // values would carry their rounding into lse whenever a few keys
-      // dominate the row)
-      pb[i / 4][i % 4] = Half<DT>::pack(ea[i], eb[i]);
-      if (i % 2 == 0) lsum_even += ea[i] + eb[i];
-      else lsum_odd += ea[i] + eb[i];
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    __builtin_amdgcn_s_setprio(0);
-    lsum = lsum_even + lsum_odd;
-
-    // exact path (rare): the running maximum rises
-    if (__any(lsum > kPmax)) {
-      const float m_blk = row_max(s) * p.c;
-      const float m_new = fmaxf(m_run, m_blk);
-      const float alpha = (m_run == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
-#pragma unroll
-      for (int mt = 0; mt < NMT; ++mt) oacc[mt] *= alpha;
-      l_run *= alpha;
-      m_run = m_new;
-      mu = (m_run == -INFINITY) ? 0.f : m_run;
-      lsum = 0.f;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) exp_chunk(i);
-    }
-    l_run += lsum;
-
-    // Straight-line region 2: GEMM-II, O^T += V^T P^T
-#pragma unroll
-    for (int t = 0; t < NV; ++t) {
-      const u32x4 a = vring[t % AHEAD];
-      if (t + AHEAD < NV) vring[t % AHEAD] = v_frag(t + AHEAD);
-      oacc[t % NMT] = Half<DT>::mfma(a, pb[t / NMT], oacc[t % NMT]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  };
-
-  // Pipeline, iteration j (P = j % 2): K(j+1) is in K buffer 1-P, V(j) in V
-  // buffer P, the scores of block j are in registers.  Issue the loads of
-  // K(j+2) into K buffer P (last read by GEMM-I of block j, an iteration ago)
-  // and V(j+1) into V buffer 1-P (last read by GEMM-II of block j-1); run
-  // GEMM-I of block j+1 alongside the softmax of block j; GEMM-II of block j.
-  // One barrier per iteration publishes the loads and retires the reads.
-  // Blocks a wave skips (causal) come only after all the blocks it computes.
-  f32x16 sa[2], sb[2];
-  auto iteration = [&](auto parity, int j, f32x16 (&s_cur)[2], f32x16 (&s_next)[2]) {
-    constexpr int P = decltype(parity)::value;
-    if (j + 2 < nkv) load_k((j + 2) * kBN, P);
-    if (j + 1 < nkv) load_v((j + 1) * kBN, 1 - P);
-    if (active(j)) block(j, 1 - P, P, s_cur, s_next);
+    load_k(0, 0);
+    load_v(0, 0);
+    if (nkv > 1) load_k(kBN, 1);
     __builtin_amdgcn_s_waitcnt(kWaitLoads);
     __syncthreads();
-  };
+    if (active(0)) gemm1(0, sa);
+    __syncthreads();   // K buffer 0 is refilled in the first iteration
 
-  load_k(0, 0);
-  load_v(0, 0);
-  if (nkv > 1) load_k(kBN, 1);
-  __builtin_amdgcn_s_waitcnt(kWaitLoads);
-  __syncthreads();
-  if (active(0)) gemm1(0, sa);
-  __syncthreads();   // K buffer 0 is refilled in the first iteration
-
-  for (int j = 0; j < nkv; j += 2) {
-    iteration(std::integral_constant<int, 0>{}, j, sa, sb);
-    if (j + 1 < nkv) iteration(std::integral_constant<int, 1>{}, j + 1, sb, sa);
-  }
-
-  // ---- epilogue: O = O / l in the storage type, lse in natural log ----
-  const float l_tot = sum_across_halves(l_run);
-  const float inv = 1.0f / l_tot;
-  const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.o + head, head_bytes);
-#pragma unroll
-  for (int mt = 0; mt < NMT; ++mt) {
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const u32x2 w = {Half<DT>::pack(oacc[mt][4 * g] * inv, oacc[mt][4 * g + 1] * inv),
-                       Half<DT>::pack(oacc[mt][4 * g + 2] * inv, oacc[mt][4 * g + 3] * inv)};
-      __builtin_amdgcn_raw_buffer_store_b64(w, ro, (uint32_t)(qrow * D + 32 * mt + 8 * g + 4 * hi) * 2, 0, 0);
+    for (int j = 0; j < nkv; j += 2) {
+      iteration(std::integral_constant<int, 0>{}, j, sa, sb);
+      if (j + 1 < nkv) iteration(std::integral_constant<int, 1>{}, j + 1, sb, sa);
     }
-  }
-  if (hi == 0) {
-    const __amdgpu_buffer_rsrc_t rl = make_rsrc(p.lse + (size_t)bh * N, (uint32_t)N * 4);
-    const float lse = (m_run + log2f(l_tot)) * 0.69314718055994531f;
-    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, lse), rl, (uint32_t)qrow * 4, 0, 0);
-  }
+
+    // ---- epilogue: O = O / l in the storage type, lse in natural log ----
+    const float l_tot = sum_across_halves(l_run);
+    const float inv = 1.0f / l_tot;
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.o + head, head_bytes);
+  #pragma unroll
+    for (int mt = 0; mt < NMT; ++mt) {
+  #pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const u32x2 w = {Half<DT>::pack(oacc[mt][4 * g] * inv, oacc[mt][4 * g + 1] * inv),
+                         Half<DT>::pack(oacc[mt][4 * g + 2] * inv, oacc[mt][4 * g + 3] * inv)};
+        __builtin_amdgcn_raw_buffer_store_b64(w, ro, (uint32_t)(qrow * D + 32 * mt + 8 * g + 4 * hi) * 2, 0, 0);
+      }
+    }
+    if (hi == 0) {
+      const __amdgpu_buffer_rsrc_t rl = make_rsrc(p.lse + (size_t)bh * N, (uint32_t)N * 4);
+      const float lse = (m_run + log2f(l_tot)) * 0.69314718055994531f;
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, lse), rl, (uint32_t)qrow * 4, 0, 0);
+    }
+  };
+  run(qbs[0]);
+  if (CAUSAL && qbs[1] >= 0) run(qbs[1]);
 }
 
 template <int D>
@@ -529,7 +541,8 @@ hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
   kp.lse = a.lse;
   kp.N = a.N;
   kp.nq = (a.N + kBM - 1) / kBM;
-  kp.total = kp.nq * a.B * a.H;
+  kp.wg_per_head = a.causal ? (kp.nq + 1) / 2 : kp.nq;
+  kp.total = kp.wg_per_head * a.B * a.H;
   kp.c = a.c;
   kp.qmode = a.qmode;
   const int key = (a.d == 128 ? 4 : 0) | (a.dtype << 1) | a.causal;

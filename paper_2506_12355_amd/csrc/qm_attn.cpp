@@ -40,10 +40,11 @@ extern "C" int qm_attn_fwd(const void* q, const void* k, const void* v, void* o,
   // workgroup count in 31 bits (the kernels index within a head in 32 bits)
   const uint64_t bh = (uint64_t)B * (uint64_t)H;
   const uint64_t nd = (uint64_t)N * (uint64_t)d;
-  // a head's byte offsets, including the padded last query block, fit in 32 bits
-  if ((uint64_t)(N + 128) * (uint64_t)d >= (1ull << 31) || bh >= (1ull << 62) / nd)
+  // a head's byte offsets, including the padded last 256-row query block, fit
+  // in 32 bits; the workgroup count fits an int
+  if ((uint64_t)(N + 256) * (uint64_t)d >= (1ull << 31) || bh >= (1ull << 62) / nd)
     return QM_ERR_SHAPE;
-  if ((uint64_t)((N + 127) / 128) * bh > (uint64_t)INT_MAX) return QM_ERR_SHAPE;
+  if ((uint64_t)((N + 255) / 256) * bh > (uint64_t)INT_MAX) return QM_ERR_SHAPE;
   if (dtype != QM_F16 && dtype != QM_BF16) return QM_ERR_DTYPE;
   if (!finite_bits(scale)) return QM_ERR_SCALE;
   if (causal != 0 && causal != 1) return QM_ERR_CAUSAL;
