@@ -77,6 +77,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 
@@ -181,13 +182,33 @@ __device__ __forceinline__ float sum_across_halves(float x) {
   return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
 }
 
-// One 16-byte-per-lane direct load HBM -> LDS: lane l's bytes at
-// voff + soff of the buffer land at lds + 16 l.  Kept out of the kernel body:
-// used there directly, the builtin makes the host pass drop the kernels'
-// launch stubs.
-__device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t rs, void* lds, uint32_t voff,
-                                           uint32_t soff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)lds, 16, voff, soff, 0, 0);
+// Buffer descriptor for the direct loads, as the four SGPRs the instruction
+// takes: base, base high bits (stride 0), size in bytes, raw 32-bit format.
+__device__ __forceinline__ i32x4 make_dma_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  return i32x4{(int32_t)__builtin_amdgcn_readfirstlane((uint32_t)b),
+               (int32_t)(__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32)) & 0xffff),
+               (int32_t)bytes, kRsrcWord3};
+}
+
+// One 16-byte-per-lane direct load HBM -> LDS: lane l's 16 bytes at byte
+// offset voff of the buffer land at LDS address lds + 16 l (M0 holds lds).
+// The whole offset is in the VGPR operand: the range check covers only that
+// operand (not the SGPR offset), and it is what turns rows past the end of
+// the sequence into zeros.
+//
+// Written as inline assembly rather than the compiler builtin: the compiler
+// cannot tell which LDS bytes a transposing read touches, so after a builtin
+// direct load it waits for every load in flight before the first V read,
+// which stalls the wave mid-block.  Here the only waits are the explicit
+// ones before each barrier.  The compiler does not resolve hazards on an
+// inline instruction's operands, so the instruction carries its own five
+// wait states: a VALU write of an SGPR (for example a spill reload of the
+// descriptor) needs five before a vector memory instruction reads it, and
+// the M0 write needs one.
+__device__ __forceinline__ void lds_load16(i32x4 rs, uint32_t lds, uint32_t voff) {
+  asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %0, %2, 0 offen lds"
+               :: "v"(voff), "{m0}"(lds), "s"(rs) : "memory");
 }
 
 template <int D, int DT, bool CAUSAL>
@@ -224,8 +245,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
   const size_t head = (size_t)bh * (size_t)N * D;
   const uint32_t head_bytes = (uint32_t)N * D * 2;
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + head, head_bytes);
-  const __amdgpu_buffer_rsrc_t rk = make_rsrc(p.k + head, head_bytes);
-  const __amdgpu_buffer_rsrc_t rv = make_rsrc(p.v + head, head_bytes);
+  const i32x4 rk = make_dma_rsrc(p.k + head, head_bytes);
+  const i32x4 rv = make_dma_rsrc(p.v + head, head_bytes);
 
   auto run = [&](int qb) __attribute__((always_inline)) {
     const int q0 = qb * kBM;
@@ -253,21 +274,23 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     // ---- HBM -> LDS: this wave's load groups of one K or V block ----
     // LDS: K buffers 0 and 1, then V buffers 0 and 1
     constexpr int VOFF = 2 * L::KBYTES;
-    // lane part of the global offset (row slot, 16-byte unit); the rest is uniform
+    // lane part of the global offset (row slot, 16-byte unit), plus the row of
+    // the load group
     const uint32_t load_lane_off = (uint32_t)(L::NG * (lane / L::U) * D * 2 + (lane % L::U) * 16);
+    auto lds_addr = [&](int byte_off) { return (uint32_t)(uintptr_t)(lds_void*)(lds + byte_off); };
     auto load_k = [&](int j0, int kb) {
   #pragma unroll
       for (int i = 0; i < GPW; ++i) {
         const int g = wave * GPW + i;
-        lds_load16(rk, lds + kb * L::KBYTES + g * L::KGS, load_lane_off, (uint32_t)((j0 + g) * D) * 2);
+        lds_load16(rk, lds_addr(kb * L::KBYTES + g * L::KGS), load_lane_off + (uint32_t)((j0 + g) * D) * 2);
       }
     };
     auto load_v = [&](int j0, int vb) {
   #pragma unroll
       for (int i = 0; i < GPW; ++i) {
         const int g = wave * GPW + i;
-        lds_load16(rv, lds + VOFF + vb * L::VBYTES + g * L::VGS, load_lane_off,
-                   (uint32_t)((j0 + g) * D) * 2);
+        lds_load16(rv, lds_addr(VOFF + vb * L::VBYTES + g * L::VGS),
+                   load_lane_off + (uint32_t)((j0 + g) * D) * 2);
       }
     };
 

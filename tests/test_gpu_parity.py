@@ -238,6 +238,32 @@ def test_every_output_written_and_nothing_else(qa):
         check_close(to_host64(o), to_host64(lse), Or, lr, "bf16", f"poisoned causal={causal}")
 
 
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("f16", 64)])
+def test_inputs_read_only_within_bounds(qa, dtype, d):
+    """Rows past the end of the sequence read as zeros: NaN placed right after the
+    last head of Q, K and V never reaches the outputs.  The guard is longer than
+    one key block, so every read stays inside the allocation either way."""
+    import torch
+    B, H, N = 2, 2, 197          # 197 = 3 * 64 + 5: the last key block has 59 missing rows
+    q, k, v = si.make_qkv(B, H, N, d, dtype, seed=12)
+    G = 2 * 64 * d
+    n = B * H * N * d
+    bufs = []
+    for x in (q, k, v):
+        t = to_device(x, dtype).reshape(-1)
+        buf = torch.full((n + G,), float("nan"), dtype=t.dtype, device="cuda")
+        buf[:n] = t
+        bufs.append(buf)
+    tq, tk, tv = (b[:n].view(B, H, N, d) for b in bufs)
+    for causal in (False, True):
+        _say(f"case guarded inputs: dtype={dtype} d={d} causal={causal}")
+        o, lse = qa.fwd(tq, tk, tv, causal=causal)
+        torch.cuda.synchronize()
+        assert bool(torch.isfinite(o).all()) and bool(torch.isfinite(lse).all())
+        Or, lr = attention_fp64(q, k, v, si.default_scale(d), causal, dtype)
+        check_close(to_host64(o), to_host64(lse), Or, lr, dtype, f"guarded inputs causal={causal}")
+
+
 def test_invalid_arguments_enqueue_nothing(qa):
     import torch
     x = torch.zeros(1, 1, 64, 96, dtype=torch.float16, device="cuda")

@@ -1,0 +1,77 @@
+"""The gfx950 kernels as compiled (CPU only: hipcc cross-compiles the device code).
+
+* every direct HBM -> LDS load is clear of the VALU-write-SGPR hazard its
+  inline assembly must resolve by itself;
+* no packed fp32 instruction appears in device code;
+* no kernel spills VGPRs or uses scratch memory.
+"""
+from __future__ import annotations
+
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2506_12355_amd import build as qbuild
+from tests.asm_hazards import dma_sgpr_hazards, instructions, is_direct_load
+
+
+@pytest.fixture(scope="module")
+def asm(tmp_path_factory):
+    try:
+        cc = qbuild.hipcc()
+    except RuntimeError:
+        pytest.skip("hipcc not available")
+    out = str(tmp_path_factory.mktemp("asm") / "attn.s")
+    flags = [f for f in qbuild.HIPCC_FLAGS if f not in ("-shared", "-fPIC")]
+    cmd = ([cc] + flags + ["--cuda-device-only", "-S", "-I", qbuild.INCLUDE, "-I", qbuild.CSRC,
+                           "-o", out, os.path.join(qbuild.CSRC, "attn_fwd_gfx950.hip")])
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    assert res.returncode == 0, res.stderr
+    return open(out).read()
+
+
+def _kernels(text):
+    """name -> instruction list, one per kernel instance."""
+    out = {}
+    for m in re.finditer(r"^(_Z\w*attn_fwd_kernel\w*):\s*(?:;.*)?$", text, flags=re.M):
+        end = text.index("s_endpgm", m.end())
+        out[m.group(1)] = instructions(text[m.end():end])
+    return out
+
+
+def test_all_instances_compiled(asm):
+    assert len(_kernels(asm)) == 8
+
+
+def test_direct_loads_have_no_sgpr_hazard(asm):
+    for name, insts in _kernels(asm).items():
+        assert any(is_direct_load(i) for i in insts), name
+        bad = dma_sgpr_hazards(insts)
+        assert not bad, f"{name}: {bad[:3]}"
+
+
+def test_no_packed_fp32(asm):
+    for name, insts in _kernels(asm).items():
+        bad = [i for i in insts if re.match(r"v_pk_(add|mul|fma|mov)_f32", i)]
+        assert not bad, f"{name}: {bad[:3]}"
+
+
+def test_no_spills_or_scratch(asm):
+    spills = [int(x) for x in re.findall(r"\.vgpr_spill_count:\s+(\d+)", asm)]
+    scratch = [int(x) for x in re.findall(r"\.private_segment_fixed_size:\s+(\d+)", asm)]
+    assert len(spills) == 8 and max(spills) == 0
+    assert len(scratch) == 8 and max(scratch) == 0
+
+
+def test_checker_sees_a_planted_hazard():
+    """The hazard scan itself: a VALU write of a descriptor SGPR two instructions
+    before a direct load is reported; five wait states in between clear it."""
+    bad = ["v_readlane_b32 s5, v243, 3", "s_mov_b32 s0, 0",
+           "buffer_load_dwordx4 v1, s[4:7], 0 offen lds"]
+    assert len(dma_sgpr_hazards(bad)) == 1
+    ok = ["v_readlane_b32 s5, v243, 3", "s_nop 4", "buffer_load_dwordx4 v1, s[4:7], 0 offen lds"]
+    assert dma_sgpr_hazards(ok) == []
+    other = ["v_readlane_b32 s9, v243, 3", "buffer_load_dwordx4 v1, s[4:7], 0 offen lds"]
+    assert dma_sgpr_hazards(other) == []
