@@ -72,8 +72,9 @@ def committed_traffic():
 class SclkSampler:
     """Samples the current SCLK with rocm-smi while the timed steps run."""
 
-    def __init__(self, period_s=0.2):
+    def __init__(self, period_s=0.2, enabled=True):
         import threading
+        self.enabled = enabled
         self.period_s = period_s
         self.samples = []
         self._stop = threading.Event()
@@ -101,12 +102,14 @@ class SclkSampler:
             self._stop.wait(self.period_s)
 
     def __enter__(self):
-        self._thread.start()
+        if self.enabled:
+            self._thread.start()
         return self
 
     def __exit__(self, *exc):
         self._stop.set()
-        self._thread.join(timeout=15)
+        if self.enabled:
+            self._thread.join(timeout=15)
 
     def median(self):
         if not self.samples:
@@ -160,6 +163,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the CPU oracle leg (for profiler runs)")
+    ap.add_argument("--no-sclk", action="store_true",
+                    help="do not sample the shader clock (rocm-smi child processes); for runs "
+                         "under a profiler that initialises the GPU in every process")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -212,7 +218,7 @@ def main():
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)]
               for _ in range(args.steps)]
     torch.cuda.synchronize(dev)
-    with SclkSampler() as sclk:
+    with SclkSampler(enabled=not args.no_sclk) as sclk:
         t0 = time.perf_counter()
         for i in range(args.steps):
             step(events[i])

@@ -32,10 +32,11 @@
 //
 // Pipeline: K and V blocks go HBM -> LDS with direct buffer loads
 // (buffer_load_dwordx4 ... lds; rows past the end of the sequence read as
-// zeros), K one block further ahead than V.  While the exponentials of block
-// j are formed, the MFMAs of GEMM-I for block j+1 run beside them (16
-// interleaved slots, the exponentials software-pipelined three deep, the wave
-// at raised issue priority); then GEMM-II of block j.  One barrier per block.
+// zeros) into four-block rings, K one block further ahead than V, each wave's
+// loads spread over its MFMA slots.  While the exponentials of block j are
+// formed, the MFMAs of GEMM-I for block j+1 run beside them (16 interleaved
+// slots, the exponentials software-pipelined three deep, the wave at raised
+// issue priority); then GEMM-II of block j.  One barrier per two blocks.
 //
 // Online softmax (exp2 domain, c = |scale| * log2 e): probabilities
 // p = 2^(c s - m) are formed against the running maximum m without first
@@ -247,6 +248,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + head, head_bytes);
   const i32x4 rk = make_dma_rsrc(p.k + head, head_bytes);
   const i32x4 rv = make_dma_rsrc(p.v + head, head_bytes);
+  // zero-size descriptors: a load through one touches no memory and writes zeros
+  const i32x4 rk0 = i32x4{rk[0], rk[1], 0, rk[3]};
+  const i32x4 rv0 = i32x4{rv[0], rv[1], 0, rv[3]};
 
   auto run = [&](int qb) __attribute__((always_inline)) {
     const int q0 = qb * kBM;
@@ -272,8 +276,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     float l_run = 0.f;         // this lane's share of the running row sum
 
     // ---- HBM -> LDS: this wave's load groups of one K or V block ----
-    // LDS: K buffers 0 and 1, then V buffers 0 and 1
-    constexpr int VOFF = 2 * L::KBYTES;
+    // LDS: four K slots, then four V slots, of one 64-key block each
+    constexpr int VOFF = 4 * L::KBYTES;
     // lane part of the global offset (row slot, 16-byte unit), plus the row of
     // the load group
     const uint32_t load_lane_off = (uint32_t)(L::NG * (lane / L::U) * D * 2 + (lane % L::U) * 16);
@@ -291,6 +295,27 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
         const int g = wave * GPW + i;
         lds_load16(rv, lds_addr(VOFF + vb * L::VBYTES + g * L::VGS),
                    load_lane_off + (uint32_t)((j0 + g) * D) * 2);
+      }
+    };
+
+    // Direct load n (of 2 GPW) issued during block j, Q = j % 4: an even block
+    // loads K(j+3) and K(j+4) into K slots (Q+3) % 4 and Q, an odd block V(j+1)
+    // and V(j+2) into V slots (Q+1) % 4 and (Q+2) % 4, GPW groups each.  Loads of
+    // blocks past the last go through the zero-size descriptor (into slots no
+    // one reads again).
+    auto dma = [&](auto ph, int n, int j) __attribute__((always_inline)) {
+      constexpr int Q = decltype(ph)::value;
+      const int second = n >= GPW ? 1 : 0;
+      const int g = wave * GPW + (n - second * GPW);
+      if (Q % 2 == 0) {
+        const int blk = j + 3 + second;
+        lds_load16(blk < nkv ? rk : rk0, lds_addr(((Q + 3 + second) % 4) * L::KBYTES + g * L::KGS),
+                   load_lane_off + (uint32_t)((blk * kBN + g) * D) * 2);
+      } else {
+        const int blk = j + 1 + second;
+        lds_load16(blk < nkv ? rv : rv0,
+                   lds_addr(VOFF + ((Q + 1 + second) % 4) * L::VBYTES + g * L::VGS),
+                   load_lane_off + (uint32_t)((blk * kBN + g) * D) * 2);
       }
     };
 
@@ -351,7 +376,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     // -inf) is the block's exact maximum taken, O and l rescaled and the
     // probabilities recomputed.  Results are exact either way: O and lse use
     // the same m_run.
-    auto block = [&](int j, int kb_next, int vb, f32x16 (&s)[2], f32x16 (&s_next)[2]) {
+    auto block = [&](auto ph, int j, int kb_next, int vb, f32x16 (&s)[2], f32x16 (&s_next)[2])
+        __attribute__((always_inline)) {
       const int j0 = j * kBN;
       constexpr int AHEAD = 4;
       constexpr int NG1 = 2 * NKS;        // GEMM-I MFMAs per block
@@ -439,6 +465,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
           s_next[m % 2] = Half<DT>::mfma(a, qf[m / 2], s_next[m % 2]);
         }
         if (i >= 16 - AHEAD) vring[i - (16 - AHEAD)] = v_frag(i - (16 - AHEAD));
+        // this block's direct loads, spread over the first half of the region
+        if (i % (8 / (2 * GPW)) == 0 && i / (8 / (2 * GPW)) < 2 * GPW) dma(ph, i / (8 / (2 * GPW)), j);
         if (i + 1 < 16) {
           ea[i + 1] = __builtin_amdgcn_exp2f(xa[i + 1]);
           eb[i + 1] = __builtin_amdgcn_exp2f(xb[i + 1]);
@@ -450,7 +478,12 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
         // 16-bit P^T operands; the row sum stays in fp32 (a sum of the rounded
         // values would carry their rounding into lse whenever a few keys
         // dominate the row)
-        pb[i / 4][i % 4] = Half<DT>::pack(ea[i], eb[i]);
+        // (the empty asm statement keeps the pack in this slot: left alone, the
+        // compiler sinks all 16 packs past the exact-path branch below, where
+        // no MFMA runs beside them)
+        uint32_t pk = Half<DT>::pack(ea[i], eb[i]);
+        asm volatile("" : "+v"(pk));
+        pb[i / 4][i % 4] = pk;
         if (i % 2 == 0) lsum_even += ea[i] + eb[i];
         else lsum_odd += ea[i] + eb[i];
         __builtin_amdgcn_sched_barrier(0);
@@ -484,35 +517,57 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
       }
     };
 
-    // Pipeline, iteration j (P = j % 2): K(j+1) is in K buffer 1-P, V(j) in V
-    // buffer P, the scores of block j are in registers.  Issue the loads of
-    // K(j+2) into K buffer P (last read by GEMM-I of block j, an iteration ago)
-    // and V(j+1) into V buffer 1-P (last read by GEMM-II of block j-1); run
-    // GEMM-I of block j+1 alongside the softmax of block j; GEMM-II of block j.
-    // One barrier per iteration publishes the loads and retires the reads.
-    // Blocks a wave skips (causal) come only after all the blocks it computes.
+    // Pipeline.  Block j (Q = j % 4) finds K(j+1) in K slot (Q+1) % 4 and V(j)
+    // in V slot Q, and issues the direct loads of the pair of blocks after the
+    // next (see dma above).  One barrier per pair of blocks, after each odd
+    // block: it publishes the pair's loads (each wave first waits for its own)
+    // and retires the pair's reads of the slots the next pair refills.  So
+    // the rings hold four blocks: two being read, two being loaded.  Blocks a
+    // wave skips (causal) come only after all the blocks it computes; it still
+    // issues their loads.
     f32x16 sa[2], sb[2];
-    auto iteration = [&](auto parity, int j, f32x16 (&s_cur)[2], f32x16 (&s_next)[2]) {
-      constexpr int P = decltype(parity)::value;
-      if (j + 2 < nkv) load_k((j + 2) * kBN, P);
-      if (j + 1 < nkv) load_v((j + 1) * kBN, 1 - P);
-      if (active(j)) block(j, 1 - P, P, s_cur, s_next);
+    auto sync = [&]() __attribute__((always_inline)) {
       __builtin_amdgcn_s_waitcnt(kWaitLoads);
       __syncthreads();
+    };
+    auto iteration = [&](auto ph, int j, f32x16 (&s_cur)[2], f32x16 (&s_next)[2])
+        __attribute__((always_inline)) {
+      constexpr int Q = decltype(ph)::value;
+      if (active(j)) {
+        block(ph, j, (Q + 1) % 4, Q, s_cur, s_next);
+      } else {
+  #pragma unroll
+        for (int n = 0; n < 2 * GPW; ++n) dma(ph, n, j);
+      }
+      if (Q % 2 == 1) sync();
     };
 
     load_k(0, 0);
     load_v(0, 0);
     if (nkv > 1) load_k(kBN, 1);
+    if (nkv > 2) load_k(2 * kBN, 2);
+    if (nkv > 1) load_v(kBN, 1);
     __builtin_amdgcn_s_waitcnt(kWaitLoads);
     __syncthreads();
     if (active(0)) gemm1(0, sa);
-    __syncthreads();   // K buffer 0 is refilled in the first iteration
+    __syncthreads();   // K slot 0 is refilled by block 0
 
-    for (int j = 0; j < nkv; j += 2) {
-      iteration(std::integral_constant<int, 0>{}, j, sa, sb);
-      if (j + 1 < nkv) iteration(std::integral_constant<int, 1>{}, j + 1, sb, sa);
+    using C0 = std::integral_constant<int, 0>;
+    using C1 = std::integral_constant<int, 1>;
+    using C2 = std::integral_constant<int, 2>;
+    using C3 = std::integral_constant<int, 3>;
+    for (int j = 0; j < nkv; j += 4) {
+      iteration(C0{}, j, sa, sb);
+      if (j + 1 >= nkv) break;
+      iteration(C1{}, j + 1, sb, sa);
+      if (j + 2 >= nkv) break;
+      iteration(C2{}, j + 2, sa, sb);
+      if (j + 3 >= nkv) break;
+      iteration(C3{}, j + 3, sb, sa);
     }
+    // a lone last block still ends with a barrier (kept out of the loop: a
+    // barrier on a loop exit path makes the register allocator spill)
+    if (nkv % 2 == 1) sync();
 
     // ---- epilogue: O = O / l in the storage type, lse in natural log ----
     const float l_tot = sum_across_halves(l_run);
@@ -539,7 +594,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
 
 template <int D>
 constexpr size_t lds_bytes() {
-  return 2 * (size_t)(Layout<D>::KBYTES + Layout<D>::VBYTES);
+  return 4 * (size_t)(Layout<D>::KBYTES + Layout<D>::VBYTES);
 }
 
 template <int D, int DT, bool CAUSAL>
