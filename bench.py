@@ -1,23 +1,27 @@
 """Throughput of the fused attention forward on one MI355X.
 
-Workload: B=2, H=32, N=8192, d=128, bf16, Q/K/V i.i.d. N(0,1) (seed 0),
+Default workload: B=2, H=32, N=8192, d=128, bf16, Q/K/V i.i.d. N(0,1) (seed 0),
 scale = 1/sqrt(d).  One step = one unmasked forward plus one causal forward
 over that batch (the two runs the workload is quoted on).  Inputs are resident
-in HBM before the timed region starts.
+in HBM before the timed region starts.  ``--workload NAME`` measures another
+named workload of ``seeded_inputs.WORKLOADS`` the same way (one forward per
+mask it lists), e.g. the grouped-query ones.
 
 Metric: TFLOPS with the paper's count, 4*B*H*N^2*d per forward (Evaluation
 section, "Benchmark setting"), halved for the causal run, summed over the
 step and divided by the wall time of the step.
 
 Prints one JSON line.  Extra objects:
-  roofline      the dominant kernel (the unmasked forward): its algorithmic
+  roofline      the dominant kernel (the first mask's forward: unmasked for
+                the default workload): its algorithmic
                 flops per launch over its mean launch duration, timed with
                 HIP events on the launch stream inside the timed region,
                 against the dense bf16 MFMA peak; ``traffic`` is the HBM bytes
                 per launch from rocprofv3 FETCH_SIZE + WRITE_SIZE counters
                 (scaled by a plain copy of known size), read from the
-                committed profile summary, or null once the kernel source has
-                changed since those counters were taken;
+                committed profile summary (default workload only), or null
+                once the kernel source has changed since those counters were
+                taken;
   cpu_baseline  the fp64 CPU oracle timed on this host on a bounded sample of
                 the same workload (whole heads, both masks), in the same unit.
 """
@@ -112,7 +116,9 @@ class SclkSampler:
             self._thread.join(timeout=15)
 
     def median(self):
-        if not self.samples:
+        # fewer than three readings means the timed region was shorter than a
+        # couple of rocm-smi calls: the readings may come from idle time
+        if len(self.samples) < 3:
             return None
         v = sorted(self.samples)
         return v[len(v) // 2]
@@ -124,10 +130,10 @@ class SclkSampler:
 def _oracle_head(args):
     from threadpoolctl import threadpool_limits
     from oracle import attention_fp64
-    q, k, v, scale, dtype = args
+    q, k, v, scale, dtype, masks = args
     with threadpool_limits(limits=1):
         t0 = time.perf_counter()
-        for causal in (False, True):
+        for causal in masks:
             attention_fp64(q, k, v, scale, causal, dtype)
         return time.perf_counter() - t0
 
@@ -136,21 +142,24 @@ def cpu_baseline(w, q, k, v, max_workers=16):
     import multiprocessing as mp
     cores = max(1, min(max_workers, len(os.sched_getaffinity(0))))
     n_heads = min(w.B * w.H, 4 * cores)
+    group = w.H // w.kv_heads
     heads = [(i // w.H, i % w.H) for i in range(n_heads)]
-    jobs = [(q[b:b + 1, h:h + 1].copy(), k[b:b + 1, h:h + 1].copy(),
-             v[b:b + 1, h:h + 1].copy(), w.scale, w.dtype) for b, h in heads]
+    jobs = [(q[b:b + 1, h:h + 1].copy(), k[b:b + 1, h // group:h // group + 1].copy(),
+             v[b:b + 1, h // group:h // group + 1].copy(), w.scale, w.dtype, w.causal)
+            for b, h in heads]
     ctx = mp.get_context("fork")
     t0 = time.perf_counter()
     with ctx.Pool(cores) as pool:
         pool.map(_oracle_head, jobs, chunksize=1)
     wall = time.perf_counter() - t0
-    work = len(heads) * (flops(1, 1, w.N, w.d, False) + flops(1, 1, w.N, w.d, True))
+    work = len(heads) * sum(flops(1, 1, w.N, w.d, c) for c in w.causal)
+    masks = "both masks" if len(w.causal) == 2 else ("causal" if w.causal[0] else "unmasked")
     return {
         "value": round(work / wall / 1e12, 6),
         "unit": "TFLOPS",
         "cores": cores,
         "kind": "oracle",
-        "sample": (f"{len(heads)} of {w.B * w.H} (batch, head) slices of {w.name}, both masks, "
+        "sample": (f"{len(heads)} of {w.B * w.H} (batch, head) slices of {w.name}, {masks}, "
                    f"spread over {cores} processes with single-threaded BLAS; wall {wall:.1f} s"),
     }
 
@@ -166,6 +175,8 @@ def main():
     ap.add_argument("--no-sclk", action="store_true",
                     help="do not sample the shader clock (rocm-smi child processes); for runs "
                          "under a profiler that initialises the GPU in every process")
+    ap.add_argument("--workload", default=si.BENCH_WORKLOAD, choices=sorted(si.WORKLOADS),
+                    help="named workload (default: the one the metric is quoted on)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -186,36 +197,35 @@ def main():
         sys.exit(1)
     qa.load_library()
 
-    w = si.WORKLOADS[si.BENCH_WORKLOAD]
+    w = si.WORKLOADS[args.workload]
     q, k, v = w.inputs()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    tdtype = torch.bfloat16 if w.dtype == "bf16" else torch.float16
 
     def dev16(x):
-        return torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(x.view(np.int16)).to(dev).view(tdtype)
 
     tq, tk, tv = dev16(q), dev16(k), dev16(v)
-    o_nc = torch.empty_like(tq)
-    o_c = torch.empty_like(tq)
-    l_nc = torch.empty((w.B, w.H, w.N), dtype=torch.float32, device=dev)
-    l_c = torch.empty_like(l_nc)
+    masks = list(w.causal)
+    outs = [(torch.empty_like(tq), torch.empty((w.B, w.H, w.N), dtype=torch.float32, device=dev))
+            for _ in masks]
     stream = torch.cuda.current_stream(dev)
 
     def step(ev=None):
+        for m, causal in enumerate(masks):
+            if ev is not None:
+                ev[m].record(stream)
+            qa.fwd(tq, tk, tv, causal=causal, scale=w.scale, out=outs[m][0], lse=outs[m][1],
+                   stream=stream)
         if ev is not None:
-            ev[0].record(stream)
-        qa.fwd(tq, tk, tv, causal=False, scale=w.scale, out=o_nc, lse=l_nc, stream=stream)
-        if ev is not None:
-            ev[1].record(stream)
-        qa.fwd(tq, tk, tv, causal=True, scale=w.scale, out=o_c, lse=l_c, stream=stream)
-        if ev is not None:
-            ev[2].record(stream)
+            ev[len(masks)].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize(dev)
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(masks) + 1)]
               for _ in range(args.steps)]
     torch.cuda.synchronize(dev)
     with SclkSampler(enabled=not args.no_sclk) as sclk:
@@ -225,15 +235,13 @@ def main():
         torch.cuda.synchronize(dev)
         wall = time.perf_counter() - t0
 
-    nc_ms = [e[0].elapsed_time(e[1]) for e in events]
-    c_ms = [e[1].elapsed_time(e[2]) for e in events]
-    f_nc = flops(w.B, w.H, w.N, w.d, False)
-    f_c = flops(w.B, w.H, w.N, w.d, True)
+    launch_ms = [sum(e[m].elapsed_time(e[m + 1]) for e in events) / len(events)
+                 for m in range(len(masks))]
+    launch_flops = [flops(w.B, w.H, w.N, w.d, c) for c in masks]
     ms_per_step = wall * 1e3 / args.steps
-    value = (f_nc + f_c) / (ms_per_step * 1e-3) / 1e12
-    nc_mean = sum(nc_ms) / len(nc_ms)
-    c_mean = sum(c_ms) / len(c_ms)
-    achieved = f_nc / (nc_mean * 1e-3) / 1e12
+    value = sum(launch_flops) / (ms_per_step * 1e-3) / 1e12
+    achieved = launch_flops[0] / (launch_ms[0] * 1e-3) / 1e12
+    mask_name = ["causal" if c else "unmasked" for c in masks]
 
     if args.copy_calibration:
         src = torch.empty(1 << 29, dtype=torch.int16, device=dev).fill_(1)
@@ -253,30 +261,29 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": w.dtype,
         "data": "synthetic",
         "config": {
-            "workload": f"{w.name}: unmasked + causal forward per step",
-            "B": w.B, "H": w.H, "N": w.N, "d": w.d, "dtype": w.dtype,
-            "masks": ["none", "causal"], "seed": w.seed,
+            "workload": f"{w.name}: {' + '.join(mask_name)} forward per step",
+            "B": w.B, "H": w.H, "Hkv": w.kv_heads, "N": w.N, "d": w.d, "dtype": w.dtype,
+            "masks": ["causal" if c else "none" for c in masks], "seed": w.seed,
         },
         "pct_of_peak": round(100.0 * value / PEAK_TFLOPS, 2),
         "sclk_mhz": sclk.median(),
         "pct_of_peak_at_sclk": (round(100.0 * value / (PEAK_FLOP_PER_CLK * sclk.median() * 1e6 / 1e12), 2)
                                 if sclk.median() else None),
         "per_launch": {
-            "unmasked": {"ms": round(nc_mean, 4), "tflops": round(achieved, 2)},
-            "causal": {"ms": round(c_mean, 4),
-                       "tflops": round(f_c / (c_mean * 1e-3) / 1e12, 2)},
+            name: {"ms": round(ms, 4), "tflops": round(f / (ms * 1e-3) / 1e12, 2)}
+            for name, ms, f in zip(mask_name, launch_ms, launch_flops)
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": "attn_fwd_kernel<128, bf16, unmasked>",
+            "kernel": f"attn_fwd_kernel<{w.d}, {w.dtype}, {mask_name[0]}>",
             "achieved": round(achieved, 2),
             "peak": PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_TFLOPS, 4),
-            "traffic": committed_traffic(),
+            "traffic": committed_traffic() if w.name == si.BENCH_WORKLOAD else None,
         },
     }
     if not args.no_cpu_baseline:

@@ -17,7 +17,8 @@
  * Conventions shared by every entry point:
  *   - All tensor pointers are DEVICE pointers owned by the caller.  The library
  *     never allocates, frees, retains or synchronises them.
- *   - q, k, v, o are contiguous row-major [B][H][N][d] arrays of the 16-bit type
+ *   - q and o are contiguous row-major [B][H][N][d] arrays, k and v
+ *     [B][Hkv][N][d] (Hkv = H except in qm_attn_fwd_gqa), of the 16-bit type
  *     named by `dtype`; o has the input type.  lse is a contiguous [B][H][N]
  *     float32 array.  Base pointers must be 16-byte aligned.
  *   - The call validates its arguments on the host, then enqueues one kernel on
@@ -41,11 +42,12 @@ typedef enum {
   QM_BF16 = 1  /* bfloat16 (top half of an IEEE binary32) */
 } qm_dtype_t;
 
-/* Status codes returned by qm_attn_fwd. */
+/* Status codes returned by qm_attn_fwd and qm_attn_fwd_gqa. */
 enum {
   QM_OK = 0,
   QM_ERR_NULL = -1,        /* q, k, v, o or lse is NULL */
-  QM_ERR_SHAPE = -2,       /* B, H or N < 1, or B*H*N*d does not fit in 62 bits */
+  QM_ERR_SHAPE = -2,       /* B, H or N < 1, Hkv not a divisor of H, or B*H*N*d
+                              does not fit in 62 bits */
   QM_ERR_HEADDIM = -3,     /* d is not 64 or 128 */
   QM_ERR_DTYPE = -4,       /* dtype is not QM_F16 or QM_BF16 */
   QM_ERR_SCALE = -5,       /* scale is infinite or NaN */
@@ -84,6 +86,28 @@ enum {
 int qm_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
                 int B, int H, int N, int d, float scale, int causal,
                 hipStream_t stream, int dtype);
+
+/*
+ * qm_attn_fwd_gqa - attention forward where H query heads share Hkv key/value
+ * heads: multi-query (Hkv = 1) and grouped-query attention, the variants the
+ * paper names beside multi-head attention in its Background and evaluates in
+ * its Evaluation section ("Attention variants"; the appendix table of LLM
+ * configurations: 64 query / 8 key-value heads, 128 / 8).  Query head h of a
+ * batch attends with key/value head h / (H / Hkv) of that batch: consecutive
+ * query heads form a group.  Every query head is otherwise exactly the
+ * qm_attn_fwd operation.
+ *
+ *   q, o     [B][H][N][d] of `dtype` (o [out]).
+ *   k, v     [in] device, [B][Hkv][N][d] of `dtype`.
+ *   lse      [out] device, [B][H][N] float32.
+ *   Hkv      key/value heads: 1 <= Hkv <= H and H % Hkv == 0, else
+ *            QM_ERR_SHAPE.  Hkv = H is exactly qm_attn_fwd.
+ *   all other arguments, the arithmetic, determinism and the status codes are
+ *   those of qm_attn_fwd.
+ */
+int qm_attn_fwd_gqa(const void* q, const void* k, const void* v, void* o, float* lse,
+                    int B, int H, int Hkv, int N, int d, float scale, int causal,
+                    hipStream_t stream, int dtype);
 
 /* qm_attn_strerror - a static, human-readable string for a status code. */
 const char* qm_attn_strerror(int status);

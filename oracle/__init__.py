@@ -9,6 +9,7 @@ from .softmax_attention import (  # noqa: F401
     attention_fp64,
     attention_rows_fp64,
     decode_fp64,
+    kv_head,
     scores_fp64,
     softmax_rows_fp64,
 )

@@ -24,6 +24,13 @@ definition written out, per (batch, head):
    (:func:`softmax_rows_fp64`);
 5. O = P V (:func:`attention_fp64`).
 
+Grouped-query and multi-query attention (named beside multi-head attention in
+the same Background subsection, and evaluated in the Evaluation section): H
+query heads share Hkv key/value heads.  The paper does not spell out the
+grouping; the reading here is the contiguous one, query head h using
+key/value head h // (H / Hkv) (:func:`kv_head`).  Each query head is then
+exactly the definition above with its group's K and V.
+
 Queries are processed in independent row blocks only to bound memory; each
 row's value is the definition's.  There is no online rescaling, no key
 blocking and no fusion.
@@ -62,6 +69,13 @@ def decode_fp64(x: np.ndarray, dtype: str) -> np.ndarray:
     raise ValueError(f"unknown dtype {dtype!r}; expected one of {_F64_DTYPES}")
 
 
+def kv_head(h: int, H: int, Hkv: int) -> int:
+    """Key/value head read by query head ``h`` when H query heads share Hkv."""
+    if Hkv < 1 or H % Hkv != 0:
+        raise ValueError(f"{Hkv} key/value heads cannot be shared by {H} query heads")
+    return h // (H // Hkv)
+
+
 def scores_fp64(Q: np.ndarray, K: np.ndarray, scale: float, causal: bool,
                 row0: int = 0) -> np.ndarray:
     """Masked scaled scores for one (batch, head).
@@ -95,20 +109,22 @@ def softmax_rows_fp64(S: np.ndarray):
 
 def attention_fp64(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float,
                    causal: bool, dtype: str, row_block: int = 256):
-    """Exact attention forward for every (batch, head) of [B, H, N, d] inputs.
+    """Exact attention forward for every (batch, head): q [B, H, N, d], k and v
+    [B, Hkv, N, d] with Hkv dividing H (Hkv = H: multi-head attention).
 
     Returns (O [B, H, N, d] fp64, lse [B, H, N] fp64).
     """
     B, H, N, d = q.shape
-    if k.shape != (B, H, N, d) or v.shape != (B, H, N, d):
-        raise ValueError("q, k, v must share the shape [B, H, N, d]")
+    Hkv = k.shape[1] if k.ndim == 4 else -1
+    if k.shape != (B, Hkv, N, d) or v.shape != (B, Hkv, N, d):
+        raise ValueError("k and v must share the shape [B, Hkv, N, d] with q's B, N, d")
     scale64 = float(np.float32(scale)) if dtype != "f64" else float(scale)
     O = np.empty((B, H, N, d), dtype=np.float64)
     lse = np.empty((B, H, N), dtype=np.float64)
     for b in range(B):
         for h in range(H):
-            K = decode_fp64(k[b, h], dtype)
-            V = decode_fp64(v[b, h], dtype)
+            K = decode_fp64(k[b, kv_head(h, H, Hkv)], dtype)
+            V = decode_fp64(v[b, kv_head(h, H, Hkv)], dtype)
             for r0 in range(0, N, row_block):
                 r1 = min(N, r0 + row_block)
                 Q = decode_fp64(q[b, h, r0:r1], dtype)
@@ -129,7 +145,8 @@ def attention_rows_fp64(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: floa
     query against all of its (visible) keys.
     """
     rows = [tuple(int(t) for t in r) for r in rows]
-    d = q.shape[-1]
+    H, d = q.shape[1], q.shape[-1]
+    Hkv = k.shape[1]
     O = np.empty((len(rows), d), dtype=np.float64)
     lse = np.empty(len(rows), dtype=np.float64)
     scale64 = float(np.float32(scale)) if dtype != "f64" else float(scale)
@@ -137,8 +154,8 @@ def attention_rows_fp64(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: floa
     for idx, (b, h, i) in enumerate(rows):
         by_head.setdefault((b, h), []).append((idx, i))
     for (b, h), items in by_head.items():
-        K = decode_fp64(k[b, h], dtype)
-        V = decode_fp64(v[b, h], dtype)
+        K = decode_fp64(k[b, kv_head(h, H, Hkv)], dtype)
+        V = decode_fp64(v[b, kv_head(h, H, Hkv)], dtype)
         for idx, i in items:
             Q = decode_fp64(q[b, h, i:i + 1], dtype)
             S = scores_fp64(Q, K, scale64, causal, row0=i)

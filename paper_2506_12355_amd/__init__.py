@@ -1,7 +1,8 @@
 """MI355X-native fused attention forward: gfx950 HIP kernels behind a C ABI.
 
 ``fwd(q, k, v, causal, scale)`` computes softmax(mask(scale * Q K^T)) V and the
-per-row log-sum-exp for [B, H, N, d] fp16/bf16 tensors on one GPU.  The
+per-row log-sum-exp for [B, H, N, d] fp16/bf16 tensors on one GPU; k and v may
+have fewer heads than q (grouped-query and multi-query attention).  The
 operation and its arguments are documented in ``include/qm_attn.h``.
 """
 from .binding import (  # noqa: F401
@@ -22,5 +23,6 @@ from .binding import (  # noqa: F401
     fwd,
     load_library,
     qm_attn_fwd,
+    qm_attn_fwd_gqa,
     strerror,
 )

@@ -58,6 +58,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
             ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
         ]
         lib.qm_attn_fwd.restype = ctypes.c_int
+        lib.qm_attn_fwd_gqa.argtypes = [
+            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+            ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+            ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+        ]
+        lib.qm_attn_fwd_gqa.restype = ctypes.c_int
         lib.qm_attn_strerror.argtypes = [ctypes.c_int]
         lib.qm_attn_strerror.restype = ctypes.c_char_p
         _lib = lib
@@ -74,6 +80,12 @@ def qm_attn_fwd(q, k, v, o, lse, B, H, N, d, scale, causal, stream, dtype) -> in
                                       float(scale), int(causal), stream, int(dtype))
 
 
+def qm_attn_fwd_gqa(q, k, v, o, lse, B, H, Hkv, N, d, scale, causal, stream, dtype) -> int:
+    """The grouped-query C entry point with plain integers for pointers; returns the status."""
+    return load_library().qm_attn_fwd_gqa(q, k, v, o, lse, int(B), int(H), int(Hkv), int(N),
+                                          int(d), float(scale), int(causal), stream, int(dtype))
+
+
 def _dtype_code(t) -> int:
     import torch
     if t.dtype == torch.float16:
@@ -85,18 +97,23 @@ def _dtype_code(t) -> int:
 
 def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse=None,
         stream=None):
-    """Attention forward on torch tensors of shape [B, H, N, d] on a ROCm device.
+    """Attention forward on torch tensors on a ROCm device.
 
-    Returns (o, lse): o has q's shape and dtype, lse is float32 [B, H, N].
-    ``scale`` defaults to 1/sqrt(d) rounded to float32.  ``stream`` defaults
-    to the current stream of q's device.
+    q is [B, H, N, d]; k and v are [B, Hkv, N, d] with Hkv dividing H (Hkv = H:
+    multi-head attention through ``qm_attn_fwd``; otherwise grouped-query or
+    multi-query attention through ``qm_attn_fwd_gqa``).  Returns (o, lse): o
+    has q's shape and dtype, lse is float32 [B, H, N].  ``scale`` defaults to
+    1/sqrt(d) rounded to float32.  ``stream`` defaults to the current stream of
+    q's device.
     """
     import torch
 
     if q.dim() != 4:
         raise ValueError("q must have shape [B, H, N, d]")
-    if k.shape != q.shape or v.shape != q.shape:
-        raise ValueError("q, k and v must have the same shape")
+    if k.dim() != 4 or v.shape != k.shape:
+        raise ValueError("k and v must have the same shape [B, Hkv, N, d]")
+    if k.shape[0] != q.shape[0] or k.shape[2:] != q.shape[2:]:
+        raise ValueError("k and v must match q in B, N and d")
     if not (q.is_cuda and k.is_cuda and v.is_cuda):
         raise ValueError("q, k and v must be on a ROCm device")
     if not (q.device == k.device == v.device):
@@ -119,10 +136,16 @@ def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse
         raise ValueError("lse must be a contiguous float32 tensor of shape [B, H, N]")
     if stream is None:
         stream = torch.cuda.current_stream(q.device)
+    Hkv = k.shape[1]
     with torch.cuda.device(q.device):
-        status = qm_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
-                             lse.data_ptr(), B, H, N, d, scale, 1 if causal else 0,
-                             stream.cuda_stream, code)
+        if Hkv == H:
+            status = qm_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                 lse.data_ptr(), B, H, N, d, scale, 1 if causal else 0,
+                                 stream.cuda_stream, code)
+        else:
+            status = qm_attn_fwd_gqa(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                     lse.data_ptr(), B, H, Hkv, N, d, scale,
+                                     1 if causal else 0, stream.cuda_stream, code)
     if status != QM_OK:
         raise QmAttnError(status, strerror(status))
     return out, lse

@@ -102,6 +102,9 @@ struct KParams {
   uint16_t* o;
   float* lse;
   int N;
+  int H;            // query heads
+  int Hkv;          // key/value heads
+  int group;        // H / Hkv: query heads per key/value head
   int nq;           // query blocks per head
   int wg_per_head;  // workgroups per head: nq, or ceil(nq / 2) pairs when causal
   int total;        // wg_per_head * B * H workgroups
@@ -243,11 +246,18 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     qbs[1] = (slot_in_head != p.nq - 1 - slot_in_head) ? slot_in_head : -1;
   }
 
+  // query head h of batch b reads key/value head h / group (grouped-query
+  // attention; group = 1 is multi-head attention).  Consecutive query heads
+  // share a key/value head, so with the id order above a whole group's
+  // workgroups run on one XCD and share its L2 for the K/V stream.
+  const int b = bh / p.H;
+  const int bhkv = b * p.Hkv + (bh - b * p.H) / p.group;
   const size_t head = (size_t)bh * (size_t)N * D;
+  const size_t head_kv = (size_t)bhkv * (size_t)N * D;
   const uint32_t head_bytes = (uint32_t)N * D * 2;
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + head, head_bytes);
-  const i32x4 rk = make_dma_rsrc(p.k + head, head_bytes);
-  const i32x4 rv = make_dma_rsrc(p.v + head, head_bytes);
+  const i32x4 rk = make_dma_rsrc(p.k + head_kv, head_bytes);
+  const i32x4 rv = make_dma_rsrc(p.v + head_kv, head_bytes);
   // zero-size descriptors: a load through one touches no memory and writes zeros
   const i32x4 rk0 = i32x4{rk[0], rk[1], 0, rk[3]};
   const i32x4 rv0 = i32x4{rv[0], rv[1], 0, rv[3]};
@@ -618,6 +628,9 @@ hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
   kp.o = a.o;
   kp.lse = a.lse;
   kp.N = a.N;
+  kp.H = a.H;
+  kp.Hkv = a.Hkv;
+  kp.group = a.H / a.Hkv;
   kp.nq = (a.N + kBM - 1) / kBM;
   kp.wg_per_head = a.causal ? (kp.nq + 1) / 2 : kp.nq;
   kp.total = kp.wg_per_head * a.B * a.H;

@@ -23,6 +23,7 @@ struct AttnArgs {
   uint16_t* o;
   float* lse;
   int B, H, N, d;
+  int Hkv;      // key/value heads; H % Hkv == 0, query head h reads h / (H / Hkv)
   int causal;   // 0 or 1
   int dtype;    // 0 = fp16, 1 = bf16
   float c;      // |scale| * log2(e), a normal positive float

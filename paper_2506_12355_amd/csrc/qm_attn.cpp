@@ -28,17 +28,17 @@ bool finite_bits(float x) {
   return (u & 0x7F800000u) != 0x7F800000u;
 }
 
-}  // namespace
-
-extern "C" int qm_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
-                           int B, int H, int N, int d, float scale, int causal,
-                           hipStream_t stream, int dtype) {
+// Validation and dispatch shared by both entry points: H query heads read Hkv
+// key/value heads (Hkv == H for plain multi-head attention).
+int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H,
+             int Hkv, int N, int d, float scale, int causal, hipStream_t stream, int dtype) {
   if (!q || !k || !v || !o || !lse) return QM_ERR_NULL;
-  if (B < 1 || H < 1 || N < 1) return QM_ERR_SHAPE;
+  if (B < 1 || H < 1 || N < 1 || Hkv < 1 || Hkv > H || H % Hkv != 0) return QM_ERR_SHAPE;
   if (d != 64 && d != 128) return QM_ERR_HEADDIM;
   // element counts: the whole tensor in 62 bits, one head's [N][d] slab and the
   // workgroup count in 31 bits (the kernels index within a head in 32 bits)
   const uint64_t bh = (uint64_t)B * (uint64_t)H;
+  const uint64_t bhkv = (uint64_t)B * (uint64_t)Hkv;
   const uint64_t nd = (uint64_t)N * (uint64_t)d;
   // a head's byte offsets, including the padded last 256-row query block, fit
   // in 32 bits; the workgroup count fits an int
@@ -49,12 +49,13 @@ extern "C" int qm_attn_fwd(const void* q, const void* k, const void* v, void* o,
   if (!finite_bits(scale)) return QM_ERR_SCALE;
   if (causal != 0 && causal != 1) return QM_ERR_CAUSAL;
 
-  const size_t tensor_bytes = (size_t)(bh * nd) * 2;
+  const size_t q_bytes = (size_t)(bh * nd) * 2;
+  const size_t kv_bytes = (size_t)(bhkv * nd) * 2;
   const size_t lse_bytes = (size_t)(bh * (uint64_t)N) * sizeof(float);
-  if (overlaps(o, tensor_bytes, q, tensor_bytes) || overlaps(o, tensor_bytes, k, tensor_bytes) ||
-      overlaps(o, tensor_bytes, v, tensor_bytes) || overlaps(lse, lse_bytes, q, tensor_bytes) ||
-      overlaps(lse, lse_bytes, k, tensor_bytes) || overlaps(lse, lse_bytes, v, tensor_bytes) ||
-      overlaps(lse, lse_bytes, o, tensor_bytes))
+  if (overlaps(o, q_bytes, q, q_bytes) || overlaps(o, q_bytes, k, kv_bytes) ||
+      overlaps(o, q_bytes, v, kv_bytes) || overlaps(lse, lse_bytes, q, q_bytes) ||
+      overlaps(lse, lse_bytes, k, kv_bytes) || overlaps(lse, lse_bytes, v, kv_bytes) ||
+      overlaps(lse, lse_bytes, o, q_bytes))
     return QM_ERR_ALIAS;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse))
     return QM_ERR_UNSUPPORTED;
@@ -67,6 +68,7 @@ extern "C" int qm_attn_fwd(const void* q, const void* k, const void* v, void* o,
   a.lse = lse;
   a.B = B;
   a.H = H;
+  a.Hkv = Hkv;
   a.N = N;
   a.d = d;
   a.causal = causal;
@@ -84,11 +86,26 @@ extern "C" int qm_attn_fwd(const void* q, const void* k, const void* v, void* o,
   return qm::launch_attn_fwd(a, stream) == hipSuccess ? QM_OK : QM_ERR_LAUNCH;
 }
 
+}  // namespace
+
+extern "C" int qm_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
+                           int B, int H, int N, int d, float scale, int causal,
+                           hipStream_t stream, int dtype) {
+  return attn_fwd(q, k, v, o, lse, B, H, H, N, d, scale, causal, stream, dtype);
+}
+
+extern "C" int qm_attn_fwd_gqa(const void* q, const void* k, const void* v, void* o,
+                               float* lse, int B, int H, int Hkv, int N, int d, float scale,
+                               int causal, hipStream_t stream, int dtype) {
+  return attn_fwd(q, k, v, o, lse, B, H, Hkv, N, d, scale, causal, stream, dtype);
+}
+
 extern "C" const char* qm_attn_strerror(int status) {
   switch (status) {
     case QM_OK: return "success";
     case QM_ERR_NULL: return "a tensor pointer is NULL";
-    case QM_ERR_SHAPE: return "B, H or N is below 1, or the tensors are too large";
+    case QM_ERR_SHAPE:
+      return "B, H or N is below 1, Hkv does not divide H, or the tensors are too large";
     case QM_ERR_HEADDIM: return "head dimension d must be 64 or 128";
     case QM_ERR_DTYPE: return "dtype must be QM_F16 (0) or QM_BF16 (1)";
     case QM_ERR_SCALE: return "scale must be finite";

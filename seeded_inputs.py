@@ -9,8 +9,9 @@ stand in for its long-context workloads of the Evaluation section's
 "Benchmark setting"):
 
 * ``rng = numpy.random.default_rng(seed)`` (PCG64), seed 0 unless stated;
-* draw ``standard_normal(shape, float32)`` for Q, then K, then V, each of
-  shape ``[B, H, N, d]``;
+* draw ``standard_normal(shape, float32)`` for Q, then K, then V; Q has shape
+  ``[B, H, N, d]`` and K, V ``[B, Hkv, N, d]`` (Hkv = H unless a grouped-query
+  workload names fewer key/value heads);
 * optionally multiply Q and K by an exact power of two in fp32 (the sharper
   long-context workload uses 2);
 * round to fp16 (numpy's cast, round-to-nearest-even) or to bf16 with
@@ -49,17 +50,19 @@ def round_to_storage(x: np.ndarray, dtype: str) -> np.ndarray:
 
 
 def make_qkv(B: int, H: int, N: int, d: int, dtype: str, seed: int = 0,
-             qk_mult: float = 1.0):
-    """Draw Q, K, V of shape [B, H, N, d] and round them to ``dtype``.
+             qk_mult: float = 1.0, Hkv: int | None = None):
+    """Draw Q [B, H, N, d] and K, V [B, Hkv, N, d] and round them to ``dtype``.
 
-    Returns three contiguous arrays (``float16`` or bf16 ``uint16`` bits).
+    ``Hkv`` defaults to H.  Returns three contiguous arrays (``float16`` or
+    bf16 ``uint16`` bits).
     """
     if dtype not in DTYPES:
         raise ValueError(f"unknown dtype {dtype!r}")
+    Hkv = H if Hkv is None else Hkv
     rng = np.random.default_rng(seed)
-    shape = (B, H, N, d)
     out = []
     for name in ("q", "k", "v"):
+        shape = (B, H, N, d) if name == "q" else (B, Hkv, N, d)
         x = rng.standard_normal(shape, dtype=np.float32)
         if name in ("q", "k") and qk_mult != 1.0:
             x *= np.float32(qk_mult)
@@ -85,6 +88,11 @@ class Workload:
     causal: tuple = field(default=(False,))
     qk_mult: float = 1.0
     seed: int = 0
+    Hkv: int = 0          # key/value heads; 0 means H (multi-head attention)
+
+    @property
+    def kv_heads(self) -> int:
+        return self.Hkv or self.H
 
     @property
     def scale(self) -> float:
@@ -92,7 +100,7 @@ class Workload:
 
     def inputs(self):
         return make_qkv(self.B, self.H, self.N, self.d, self.dtype,
-                        seed=self.seed, qk_mult=self.qk_mult)
+                        seed=self.seed, qk_mult=self.qk_mult, Hkv=self.kv_heads)
 
 
 WORKLOADS = {
@@ -103,6 +111,17 @@ WORKLOADS = {
         Workload("mha_b2_h32_n8192_d128_bf16", 2, 32, 8192, 128, "bf16", (False, True)),
         Workload("mha_b1_h32_n32768_d128_bf16_causal_qk2", 1, 32, 32768, 128, "bf16",
                  (True,), qk_mult=2.0),
+        # grouped-query and multi-query attention: the appendix table's LLM head
+        # configurations (64 query / 8 key-value heads, 128 / 8; d = 128, causal)
+        # at the 16k-token budget of the benchmark grid, plus MQA and small cases
+        Workload("gqa_b2_h64_kv8_n8192_d128_bf16_causal", 2, 64, 8192, 128, "bf16", (True,),
+                 Hkv=8),
+        Workload("gqa_b2_h128_kv8_n8192_d128_bf16_causal", 2, 128, 8192, 128, "bf16", (True,),
+                 Hkv=8),
+        Workload("mqa_b2_h32_kv1_n8192_d128_bf16", 2, 32, 8192, 128, "bf16", (False, True),
+                 Hkv=1),
+        Workload("gqa_b2_h8_kv2_n1000_d64_f16", 2, 8, 1000, 64, "f16", (False, True), Hkv=2),
+        Workload("mqa_b2_h6_kv1_n777_d128_bf16", 2, 6, 777, 128, "bf16", (False, True), Hkv=1),
     )
 }
 

@@ -11,7 +11,10 @@ acceleration") fixes independently of any implementation:
 * invariants (softmax rows sum to 1, shift invariance in K, linearity in V,
   key-permutation invariance, constant value rows);
 * special cases (one key, causal row 0, causal last row, causal prefix, a
-  sharp one-hot row, large scales without overflow).
+  sharp one-hot row, large scales without overflow);
+* grouped-query attention: each query head against the brute force with its
+  group's key/value head, equality with explicitly repeated key/value heads,
+  identical query heads under multi-query attention.
 
 ``tests/test_oracle.py`` runs every pin on the oracle and shows that planted
 mistakes in the oracle fail at least one pin.
@@ -301,6 +304,69 @@ def pin_decode(mod):
         raise AssertionError(f"f16 decode {list(got)} != {expect}")
 
 
+GQA_BRUTE_CASES = [
+    # (H, Hkv, N, d, dtype, scale, causal, seed)
+    (4, 2, 5, 8, "f16", 0.4, True, 31),
+    (3, 1, 6, 4, "bf16", 0.9, False, 32),
+    (6, 3, 4, 16, "bf16", 0.25, True, 33),
+    (4, 4, 3, 4, "f16", -0.5, False, 34),
+]
+
+
+def pin_gqa_brute_force(mod):
+    """Grouped-query attention: every query head equals the 50-digit brute force
+    with the key/value head of its contiguous group, index h * Hkv // H."""
+    for H, Hkv, N, d, dtype, scale, causal, seed in GQA_BRUTE_CASES:
+        q, k, v = make_qkv(1, H, N, d, dtype, seed=seed, Hkv=Hkv)
+        O, lse = mod.attention_fp64(q, k, v, scale, causal, dtype, row_block=2)
+        s32 = float(np.float32(scale))
+        for h in range(H):
+            g = h * Hkv // H
+            qf = _decode_independent(q[0, h], dtype)
+            kf = _decode_independent(k[0, g], dtype)
+            vf = _decode_independent(v[0, g], dtype)
+            Ob, lb = brute_force_decimal(qf, kf, vf, s32, causal)
+            tol = 1e-13 * (1.0 + abs(s32) * float(np.max(np.abs(qf @ kf.T))))
+            _close(O[0, h], Ob, tol * max(1.0, float(np.max(np.abs(vf)))),
+                   f"GQA O brute H={H} Hkv={Hkv} head {h}")
+            _close(lse[0, h], lb, tol * max(1.0, float(np.max(np.abs(lb)))),
+                   f"GQA lse brute H={H} Hkv={Hkv} head {h}")
+    # the per-row entry point maps heads the same way
+    q, k, v = make_qkv(2, 6, 9, 8, "bf16", seed=35, Hkv=2)
+    O, lse = mod.attention_fp64(q, k, v, 0.3, True, "bf16")
+    rows = [(0, 0, 3), (1, 5, 8), (0, 2, 0), (1, 3, 6)]
+    Or, lr = mod.attention_rows_fp64(q, k, v, 0.3, True, "bf16", rows)
+    for t, (b, h, i) in enumerate(rows):
+        _close(Or[t], O[b, h, i], 1e-14, "GQA row entry O")
+        _close(lr[t], lse[b, h, i], 1e-14, "GQA row entry lse")
+
+
+def pin_gqa_is_mha_on_repeated_heads(mod):
+    """Sharing a key/value head is the same as giving each query head its own
+    copy: GQA on [B, Hkv] equals MHA on K, V with each head repeated H/Hkv times."""
+    for H, Hkv, causal in [(8, 2, False), (6, 1, True), (4, 4, True)]:
+        q, k, v = make_qkv(2, H, 13, 8, "f16", seed=36 + H, Hkv=Hkv)
+        O, lse = mod.attention_fp64(q, k, v, 0.35, causal, "f16", row_block=5)
+        kr = np.ascontiguousarray(np.repeat(k, H // Hkv, axis=1))
+        vr = np.ascontiguousarray(np.repeat(v, H // Hkv, axis=1))
+        Or, lr = mod.attention_fp64(q, kr, vr, 0.35, causal, "f16", row_block=5)
+        _close(O, Or, 0.0, f"GQA vs repeated heads H={H} Hkv={Hkv}")
+        _close(lse, lr, 0.0, f"GQA lse vs repeated heads H={H} Hkv={Hkv}")
+
+
+def pin_mqa_identical_query_heads(mod):
+    """Multi-query attention with every query head the same gives the same
+    output in every head, equal to single-head attention."""
+    q1, k, v = make_qkv(1, 1, 11, 16, "bf16", seed=40)
+    q = np.ascontiguousarray(np.repeat(q1, 5, axis=1))
+    for causal in (False, True):
+        O, lse = mod.attention_fp64(q, k, v, 0.25, causal, "bf16")
+        O1, l1 = mod.attention_fp64(q1, k, v, 0.25, causal, "bf16")
+        for h in range(5):
+            _close(O[0, h], O1[0, 0], 0.0, "MQA identical heads")
+            _close(lse[0, h], l1[0, 0], 0.0, "MQA identical heads lse")
+
+
 ALL_PINS = [
     pin_brute_force,
     pin_zero_query_mean,
@@ -315,4 +381,7 @@ ALL_PINS = [
     pin_one_hot,
     pin_rows_match_full,
     pin_decode,
+    pin_gqa_brute_force,
+    pin_gqa_is_mha_on_repeated_heads,
+    pin_mqa_identical_query_heads,
 ]

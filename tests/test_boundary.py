@@ -37,7 +37,7 @@ def _declared_functions():
 
 
 def test_header_declares_entry_points():
-    assert {"qm_attn_fwd", "qm_attn_strerror"} <= set(_declared_functions())
+    assert {"qm_attn_fwd", "qm_attn_fwd_gqa", "qm_attn_strerror"} <= set(_declared_functions())
 
 
 def test_library_exports_every_declared_symbol(lib):
@@ -104,6 +104,41 @@ def call(**over):
 ], ids=lambda x: str(x))
 def test_invalid_arguments_are_rejected(lib, over, status):
     assert call(**over) == status
+
+
+def call_gqa(Hkv, **over):
+    a = dict(GOOD)
+    a.update(over)
+    return qa.qm_attn_fwd_gqa(a["q"], a["k"], a["v"], a["o"], a["lse"], a["B"], a["H"], Hkv,
+                              a["N"], a["d"], a["scale"], a["causal"], a["stream"], a["dtype"])
+
+
+@pytest.mark.parametrize("H,Hkv,over,status", [
+    (8, 0, {}, qa.QM_ERR_SHAPE),
+    (8, -2, {}, qa.QM_ERR_SHAPE),
+    (8, 16, {}, qa.QM_ERR_SHAPE),                       # more key/value heads than query heads
+    (8, 3, {}, qa.QM_ERR_SHAPE),                        # does not divide H
+    (6, 4, {}, qa.QM_ERR_SHAPE),
+    (8, 2, dict(k=None), qa.QM_ERR_NULL),
+    (8, 2, dict(d=96), qa.QM_ERR_HEADDIM),
+    (8, 2, dict(dtype=5), qa.QM_ERR_DTYPE),
+    (8, 2, dict(scale=float("nan")), qa.QM_ERR_SCALE),
+    (8, 2, dict(causal=3), qa.QM_ERR_CAUSAL),
+    (8, 2, dict(o=K + 16 * 1024), qa.QM_ERR_ALIAS),       # inside k's 2-head extent
+    (8, 2, dict(lse=V + 16), qa.QM_ERR_ALIAS),
+    (8, 2, dict(v=V + 8), qa.QM_ERR_UNSUPPORTED),
+], ids=lambda x: str(x))
+def test_gqa_invalid_arguments_are_rejected(lib, H, Hkv, over, status):
+    assert call_gqa(Hkv, H=H, **over) == status
+
+
+def test_gqa_alias_extent_follows_kv_heads(lib):
+    """k and v hold Hkv heads, so o may start right after k's shorter extent.
+    A misaligned lse (checked after the alias rules) keeps anything from being
+    enqueued either way."""
+    kv_bytes = 1 * 2 * 128 * 64 * 2          # B=1, Hkv=2, N=128, d=64, 16-bit
+    assert call_gqa(2, H=8, o=K + kv_bytes, lse=L + 4) == qa.QM_ERR_UNSUPPORTED
+    assert call_gqa(8, H=8, o=K + kv_bytes, lse=L + 4) == qa.QM_ERR_ALIAS
 
 
 def test_inputs_may_alias_each_other(lib):

@@ -136,6 +136,20 @@ def _attention_last_row_block_dropped(q, k, v, scale, causal, dtype, row_block=2
     return O, lse
 
 
+_orig_kv_head = om.kv_head
+
+
+def _kv_head_modulo(h, H, Hkv):
+    # interleaved instead of contiguous groups
+    _orig_kv_head(h, H, Hkv)
+    return h % Hkv
+
+
+def _kv_head_first(h, H, Hkv):
+    _orig_kv_head(h, H, Hkv)
+    return 0
+
+
 MUTANTS = {
     "scores_no_scale": ("scores_fp64", _scores_no_scale),
     "scores_fixed_scale": ("scores_fp64", _scores_fixed_scale),
@@ -154,6 +168,8 @@ MUTANTS = {
     "decode_bf16_wrong_shift": ("decode_fp64", _decode_bf16_wrong_shift),
     "decode_f16_as_bf16": ("decode_fp64", _decode_f16_via_bf16),
     "attention_drops_tail_rows": ("attention_fp64", _attention_last_row_block_dropped),
+    "kv_head_interleaved": ("kv_head", _kv_head_modulo),
+    "kv_head_always_first": ("kv_head", _kv_head_first),
 }
 
 
