@@ -165,6 +165,46 @@ def cpu_baseline(w, q, k, v, max_workers=16):
 
 
 # --------------------------------------------------------------------------
+# the paper's benchmark grid: 16k tokens per batch, hidden 2048, d 64 / 128
+# --------------------------------------------------------------------------
+def run_grid(args, qa, torch, np):
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    for name, w in si.GRID.items():
+        q, k, v = w.inputs()
+        tq, tk, tv = (torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+                      for x in (q, k, v))
+        del q, k, v
+        o = torch.empty_like(tq)
+        lse = torch.empty((w.B, w.H, w.N), dtype=torch.float32, device=dev)
+        per = {}
+        for causal in w.causal:
+            # the C entry point directly: short launches must not wait on
+            # Python-side argument checks
+            call = (tq.data_ptr(), tk.data_ptr(), tv.data_ptr(), o.data_ptr(), lse.data_ptr(),
+                    w.B, w.H, w.N, w.d, w.scale, int(causal), stream.cuda_stream, qa.QM_BF16)
+            for _ in range(args.warmup):
+                assert qa.qm_attn_fwd(*call) == qa.QM_OK
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            ev[0].record(stream)
+            for _ in range(args.steps):
+                qa.qm_attn_fwd(*call)
+            ev[1].record(stream)
+            torch.cuda.synchronize(dev)
+            ms = ev[0].elapsed_time(ev[1]) / args.steps
+            tf = flops(w.B, w.H, w.N, w.d, causal) / (ms * 1e-3) / 1e12
+            per["causal" if causal else "unmasked"] = {
+                "ms": round(ms, 4), "tflops": round(tf, 2),
+                "pct_of_peak": round(100.0 * tf / PEAK_TFLOPS, 2)}
+        print(json.dumps({"metric": METRIC, "grid": True, "workload": name,
+                          "B": w.B, "H": w.H, "N": w.N, "d": w.d, "dtype": w.dtype,
+                          "steps": args.steps, "warmup": args.warmup, "per_launch": per}),
+              flush=True)
+        del tq, tk, tv, o, lse
+
+
+# --------------------------------------------------------------------------
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -177,6 +217,8 @@ def main():
                          "under a profiler that initialises the GPU in every process")
     ap.add_argument("--workload", default=si.BENCH_WORKLOAD, choices=sorted(si.WORKLOADS),
                     help="named workload (default: the one the metric is quoted on)")
+    ap.add_argument("--grid", action="store_true",
+                    help="measure the paper's benchmark grid instead (one JSON line per shape)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -196,6 +238,10 @@ def main():
         print("bench.py needs a ROCm GPU", file=sys.stderr)
         sys.exit(1)
     qa.load_library()
+
+    if args.grid:
+        run_grid(args, qa, torch, np)
+        return
 
     w = si.WORKLOADS[args.workload]
     q, k, v = w.inputs()

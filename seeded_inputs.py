@@ -125,6 +125,18 @@ WORKLOADS = {
     )
 }
 
+# The paper's benchmark grid (Evaluation, "Benchmark setting"): sequence length
+# 512 .. 16k at a fixed 16k tokens per batch (B = 16384 / N), hidden size 2048
+# (H = 2048 / d), head dimension 64 or 128, with and without the causal mask.
+GRID_N = (512, 1024, 2048, 4096, 8192, 16384)
+GRID_D = (64, 128)
+GRID = {
+    f"grid_d{d}_n{n}": Workload(f"grid_d{d}_n{n}", 16384 // n, 2048 // d, n, d, "bf16",
+                                (False, True))
+    for d in GRID_D for n in GRID_N
+}
+WORKLOADS.update(GRID)
+
 # The workload the throughput figure is quoted on (N = 8192, d = 128).
 BENCH_WORKLOAD = "mha_b2_h32_n8192_d128_bf16"
 # The small workload that the full oracle finishes in well under a second.

@@ -121,6 +121,26 @@ def test_long_workloads_sampled(qa, name, causal):
         assert torch.equal(lse[:, :, -1], l2[:, :, -1])
 
 
+@pytest.mark.parametrize("name", sorted(si.GRID))
+def test_paper_grid_sampled(qa, name):
+    """Every shape of the paper's benchmark grid, both masks, on sampled rows."""
+    import torch
+    w = si.GRID[name]
+    _say(f"case {name}: drawing inputs")
+    q, k, v = w.inputs()
+    tq, tk, tv = (to_device(x, w.dtype) for x in (q, k, v))
+    rows = _sample_rows(w, 24, seed=5)
+    ix = tuple(torch.tensor(np.array(rows).T).cuda())
+    for causal in w.causal:
+        _say(f"case {name} causal={causal}")
+        o, lse = qa.fwd(tq, tk, tv, causal=causal, scale=w.scale)
+        torch.cuda.synchronize()
+        assert bool(torch.isfinite(o).all()) and bool(torch.isfinite(lse).all())
+        Or, lr = attention_rows_fp64(q, k, v, w.scale, causal, w.dtype, rows)
+        check_close(to_host64(o[ix]), to_host64(lse[ix]), Or, lr, w.dtype,
+                    f"{name} causal={causal} sampled rows")
+
+
 # ---------------------------------------------------------------- edge shapes
 EDGE_N = [1, 2, 17, 63, 64, 65, 127, 128, 129, 255, 1000]
 
