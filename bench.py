@@ -48,8 +48,12 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2506_12355_amd", "csrc", "attn_fwd_gfx
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_fwd_bf16_d128_n8192_hbm_traffic.md")
 
 
-def flops(B, H, N, d, causal):
-    f = 4.0 * B * H * N * N * d
+def flops(B, H, N, d, causal, dv=None):
+    """The paper's count, 4*B*H*N^2*d, halved for causal; with a value head
+    dimension dv != d (the MLA shape) the two products count 2*B*H*N^2*d and
+    2*B*H*N^2*dv."""
+    dv = d if dv is None else dv
+    f = 2.0 * B * H * N * N * (d + dv)
     return f / 2 if causal else f
 
 
@@ -152,7 +156,7 @@ def cpu_baseline(w, q, k, v, max_workers=16):
     with ctx.Pool(cores) as pool:
         pool.map(_oracle_head, jobs, chunksize=1)
     wall = time.perf_counter() - t0
-    work = len(heads) * sum(flops(1, 1, w.N, w.d, c) for c in w.causal)
+    work = len(heads) * sum(flops(1, 1, w.N, w.d, c, w.d_v) for c in w.causal)
     masks = "both masks" if len(w.causal) == 2 else ("causal" if w.causal[0] else "unmasked")
     return {
         "value": round(work / wall / 1e12, 6),
@@ -254,7 +258,8 @@ def main():
 
     tq, tk, tv = dev16(q), dev16(k), dev16(v)
     masks = list(w.causal)
-    outs = [(torch.empty_like(tq), torch.empty((w.B, w.H, w.N), dtype=torch.float32, device=dev))
+    outs = [(torch.empty((w.B, w.H, w.N, w.d_v), dtype=tdtype, device=dev),
+             torch.empty((w.B, w.H, w.N), dtype=torch.float32, device=dev))
             for _ in masks]
     stream = torch.cuda.current_stream(dev)
 
@@ -283,7 +288,7 @@ def main():
 
     launch_ms = [sum(e[m].elapsed_time(e[m + 1]) for e in events) / len(events)
                  for m in range(len(masks))]
-    launch_flops = [flops(w.B, w.H, w.N, w.d, c) for c in masks]
+    launch_flops = [flops(w.B, w.H, w.N, w.d, c, w.d_v) for c in masks]
     ms_per_step = wall * 1e3 / args.steps
     value = sum(launch_flops) / (ms_per_step * 1e-3) / 1e12
     achieved = launch_flops[0] / (launch_ms[0] * 1e-3) / 1e12
@@ -311,7 +316,9 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": f"{w.name}: {' + '.join(mask_name)} forward per step",
-            "B": w.B, "H": w.H, "Hkv": w.kv_heads, "N": w.N, "d": w.d, "dtype": w.dtype,
+            "B": w.B, "H": w.H, "Hkv": w.kv_heads, "N": w.N, "d": w.d, "d_v": w.d_v,
+            "dtype": w.dtype,
+            "flop_count": ("4·B·H·N²·d" if w.d_v == w.d else "2·B·H·N²·(d + d_v)") + ", ½ if causal",
             "masks": ["causal" if c else "none" for c in masks], "seed": w.seed,
         },
         "pct_of_peak": round(100.0 * value / PEAK_TFLOPS, 2),
@@ -324,7 +331,7 @@ def main():
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": f"attn_fwd_kernel<{w.d}, {w.dtype}, {mask_name[0]}>",
+            "kernel": f"attn_fwd_kernel<{w.d}, {w.d_v}, {w.dtype}, {mask_name[0]}>",
             "achieved": round(achieved, 2),
             "peak": PEAK_TFLOPS,
             "unit": "TFLOP/s",

@@ -18,9 +18,10 @@
  *   - All tensor pointers are DEVICE pointers owned by the caller.  The library
  *     never allocates, frees, retains or synchronises them.
  *   - q and o are contiguous row-major [B][H][N][d] arrays, k and v
- *     [B][Hkv][N][d] (Hkv = H except in qm_attn_fwd_gqa), of the 16-bit type
- *     named by `dtype`; o has the input type.  lse is a contiguous [B][H][N]
- *     float32 array.  Base pointers must be 16-byte aligned.
+ *     [B][Hkv][N][d] (Hkv = H except in qm_attn_fwd_gqa; in qm_attn_fwd_mla
+ *     v and o have their own head dimension), of the 16-bit type named by
+ *     `dtype`; o has the input type.  lse is a contiguous [B][H][N] float32
+ *     array.  Base pointers must be 16-byte aligned.
  *   - The call validates its arguments on the host, then enqueues one kernel on
  *     `stream` (NULL = the null stream) and returns; results are valid once the
  *     caller has synchronised that stream.  On any error nothing is enqueued and
@@ -42,13 +43,14 @@ typedef enum {
   QM_BF16 = 1  /* bfloat16 (top half of an IEEE binary32) */
 } qm_dtype_t;
 
-/* Status codes returned by qm_attn_fwd and qm_attn_fwd_gqa. */
+/* Status codes returned by qm_attn_fwd, qm_attn_fwd_gqa and qm_attn_fwd_mla. */
 enum {
   QM_OK = 0,
   QM_ERR_NULL = -1,        /* q, k, v, o or lse is NULL */
   QM_ERR_SHAPE = -2,       /* B, H or N < 1, Hkv not a divisor of H, or B*H*N*d
                               does not fit in 62 bits */
-  QM_ERR_HEADDIM = -3,     /* d is not 64 or 128 */
+  QM_ERR_HEADDIM = -3,     /* d is not 64 or 128 (qm_attn_fwd_mla: (d_qk, d_v) is not
+                              (64, 64), (128, 128) or (192, 128)) */
   QM_ERR_DTYPE = -4,       /* dtype is not QM_F16 or QM_BF16 */
   QM_ERR_SCALE = -5,       /* scale is infinite or NaN */
   QM_ERR_ALIAS = -6,       /* o or lse overlaps q, k, v or each other */
@@ -107,6 +109,28 @@ int qm_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse
  */
 int qm_attn_fwd_gqa(const void* q, const void* k, const void* v, void* o, float* lse,
                     int B, int H, int Hkv, int N, int d, float scale, int causal,
+                    hipStream_t stream, int dtype);
+
+/*
+ * qm_attn_fwd_mla - attention forward with a wider query/key head than value
+ * head: the multi-head latent attention shape the paper evaluates (its MLA
+ * table: DeepSeek-V3's configuration, head dimension 128 plus a 64-wide RoPE
+ * part, so d_qk = 192 and d_v = 128, with the causal mask), taken in its
+ * explicit form where every head has its own keys and values.
+ *
+ *   q, k     [in]  device, [B][H][N][d_qk] of `dtype`.
+ *   v        [in]  device, [B][H][N][d_v] of `dtype`.
+ *   o        [out] device, [B][H][N][d_v] of `dtype`.
+ *   lse      [out] device, [B][H][N] float32.
+ *   d_qk, d_v      (192, 128); (64, 64) and (128, 128) are qm_attn_fwd.
+ *                  Any other pair: QM_ERR_HEADDIM.
+ *   scale          multiplies q_i . k_j over all d_qk columns (usually
+ *                  1/sqrt(d_qk)).
+ *   all other arguments, the arithmetic, determinism and the status codes are
+ *   those of qm_attn_fwd.
+ */
+int qm_attn_fwd_mla(const void* q, const void* k, const void* v, void* o, float* lse,
+                    int B, int H, int N, int d_qk, int d_v, float scale, int causal,
                     hipStream_t stream, int dtype);
 
 /* qm_attn_strerror - a static, human-readable string for a status code. */

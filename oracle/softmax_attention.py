@@ -37,7 +37,9 @@ blocking and no fusion.
 
 Readings where the paper is silent: the head layout is [B, H, N, d]; lse is
 the natural logarithm; the scale is applied to the exact dot product, never to
-16-bit Q.
+16-bit Q.  Values may have their own head dimension d_v (the MLA shape the
+paper evaluates: queries and keys 128 + 64 wide, values 128): the scores use
+all d columns of Q and K, the output has d_v columns.
 
 Pins: ``tests/test_oracle.py`` checks every function here against a
 high-precision brute force, closed forms, invariants and special cases, and
@@ -109,17 +111,19 @@ def softmax_rows_fp64(S: np.ndarray):
 
 def attention_fp64(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float,
                    causal: bool, dtype: str, row_block: int = 256):
-    """Exact attention forward for every (batch, head): q [B, H, N, d], k and v
-    [B, Hkv, N, d] with Hkv dividing H (Hkv = H: multi-head attention).
+    """Exact attention forward for every (batch, head): q [B, H, N, d], k
+    [B, Hkv, N, d] and v [B, Hkv, N, dv] with Hkv dividing H (Hkv = H:
+    multi-head attention).
 
-    Returns (O [B, H, N, d] fp64, lse [B, H, N] fp64).
+    Returns (O [B, H, N, dv] fp64, lse [B, H, N] fp64).
     """
     B, H, N, d = q.shape
     Hkv = k.shape[1] if k.ndim == 4 else -1
-    if k.shape != (B, Hkv, N, d) or v.shape != (B, Hkv, N, d):
-        raise ValueError("k and v must share the shape [B, Hkv, N, d] with q's B, N, d")
+    dv = v.shape[-1] if v.ndim == 4 else -1
+    if k.shape != (B, Hkv, N, d) or v.shape != (B, Hkv, N, dv):
+        raise ValueError("k must be [B, Hkv, N, d] and v [B, Hkv, N, dv] with q's B, N, d")
     scale64 = float(np.float32(scale)) if dtype != "f64" else float(scale)
-    O = np.empty((B, H, N, d), dtype=np.float64)
+    O = np.empty((B, H, N, dv), dtype=np.float64)
     lse = np.empty((B, H, N), dtype=np.float64)
     for b in range(B):
         for h in range(H):
@@ -139,15 +143,15 @@ def attention_rows_fp64(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: floa
                         causal: bool, dtype: str, rows):
     """Exact attention output for selected rows only.
 
-    ``rows``: iterable of (b, h, i).  Returns (O [R, d] fp64, lse [R] fp64) in
+    ``rows``: iterable of (b, h, i).  Returns (O [R, dv] fp64, lse [R] fp64) in
     the order given.  Used where the full output is too large for the CPU:
     each selected row is the definition's value, computed from that row's
     query against all of its (visible) keys.
     """
     rows = [tuple(int(t) for t in r) for r in rows]
-    H, d = q.shape[1], q.shape[-1]
+    H = q.shape[1]
     Hkv = k.shape[1]
-    O = np.empty((len(rows), d), dtype=np.float64)
+    O = np.empty((len(rows), v.shape[-1]), dtype=np.float64)
     lse = np.empty(len(rows), dtype=np.float64)
     scale64 = float(np.float32(scale)) if dtype != "f64" else float(scale)
     by_head = {}

@@ -2,7 +2,8 @@
 
 ``fwd(q, k, v, causal, scale)`` computes softmax(mask(scale * Q K^T)) V and the
 per-row log-sum-exp for [B, H, N, d] fp16/bf16 tensors on one GPU; k and v may
-have fewer heads than q (grouped-query and multi-query attention).  The
+have fewer heads than q (grouped-query and multi-query attention), and v a
+narrower head than q and k (the MLA shape, 192/128).  The
 operation and its arguments are documented in ``include/qm_attn.h``.
 """
 from .binding import (  # noqa: F401
@@ -24,5 +25,6 @@ from .binding import (  # noqa: F401
     load_library,
     qm_attn_fwd,
     qm_attn_fwd_gqa,
+    qm_attn_fwd_mla,
     strerror,
 )

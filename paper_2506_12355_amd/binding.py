@@ -64,6 +64,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
             ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
         ]
         lib.qm_attn_fwd_gqa.restype = ctypes.c_int
+        lib.qm_attn_fwd_mla.argtypes = [
+            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+            ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+            ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+        ]
+        lib.qm_attn_fwd_mla.restype = ctypes.c_int
         lib.qm_attn_strerror.argtypes = [ctypes.c_int]
         lib.qm_attn_strerror.restype = ctypes.c_char_p
         _lib = lib
@@ -86,6 +92,12 @@ def qm_attn_fwd_gqa(q, k, v, o, lse, B, H, Hkv, N, d, scale, causal, stream, dty
                                           int(d), float(scale), int(causal), stream, int(dtype))
 
 
+def qm_attn_fwd_mla(q, k, v, o, lse, B, H, N, d_qk, d_v, scale, causal, stream, dtype) -> int:
+    """The unequal-head-dimension C entry point with plain integers for pointers."""
+    return load_library().qm_attn_fwd_mla(q, k, v, o, lse, int(B), int(H), int(N), int(d_qk),
+                                          int(d_v), float(scale), int(causal), stream, int(dtype))
+
+
 def _dtype_code(t) -> int:
     import torch
     if t.dtype == torch.float16:
@@ -99,21 +111,22 @@ def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse
         stream=None):
     """Attention forward on torch tensors on a ROCm device.
 
-    q is [B, H, N, d]; k and v are [B, Hkv, N, d] with Hkv dividing H (Hkv = H:
-    multi-head attention through ``qm_attn_fwd``; otherwise grouped-query or
-    multi-query attention through ``qm_attn_fwd_gqa``).  Returns (o, lse): o
-    has q's shape and dtype, lse is float32 [B, H, N].  ``scale`` defaults to
-    1/sqrt(d) rounded to float32.  ``stream`` defaults to the current stream of
-    q's device.
+    q is [B, H, N, d]; k is [B, Hkv, N, d] and v [B, Hkv, N, dv] with Hkv
+    dividing H.  Hkv = H and dv = d: multi-head attention (``qm_attn_fwd``);
+    Hkv < H: grouped-query or multi-query attention (``qm_attn_fwd_gqa``);
+    dv < d (d = 192, dv = 128, Hkv = H): the MLA shape (``qm_attn_fwd_mla``).
+    Returns (o, lse): o is [B, H, N, dv] of q's dtype, lse is float32
+    [B, H, N].  ``scale`` defaults to 1/sqrt(d) rounded to float32.
+    ``stream`` defaults to the current stream of q's device.
     """
     import torch
 
     if q.dim() != 4:
         raise ValueError("q must have shape [B, H, N, d]")
-    if k.dim() != 4 or v.shape != k.shape:
-        raise ValueError("k and v must have the same shape [B, Hkv, N, d]")
+    if k.dim() != 4 or v.dim() != 4 or v.shape[:3] != k.shape[:3]:
+        raise ValueError("k must be [B, Hkv, N, d] and v [B, Hkv, N, dv]")
     if k.shape[0] != q.shape[0] or k.shape[2:] != q.shape[2:]:
-        raise ValueError("k and v must match q in B, N and d")
+        raise ValueError("k must match q in B, N and d")
     if not (q.is_cuda and k.is_cuda and v.is_cuda):
         raise ValueError("q, k and v must be on a ROCm device")
     if not (q.device == k.device == v.device):
@@ -123,13 +136,14 @@ def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse
     if not (q.is_contiguous() and k.is_contiguous() and v.is_contiguous()):
         raise ValueError("q, k and v must be contiguous [B, H, N, d]")
     B, H, N, d = q.shape
+    dv = v.shape[3]
     code = _dtype_code(q)
     if scale is None:
         scale = float(torch.tensor(1.0 / d ** 0.5, dtype=torch.float32))
     if out is None:
-        out = torch.empty_like(q)
-    elif out.shape != q.shape or out.dtype != q.dtype or not out.is_contiguous():
-        raise ValueError("out must be a contiguous tensor like q")
+        out = torch.empty((B, H, N, dv), dtype=q.dtype, device=q.device)
+    elif out.shape != (B, H, N, dv) or out.dtype != q.dtype or not out.is_contiguous():
+        raise ValueError("out must be a contiguous [B, H, N, dv] tensor of q's dtype")
     if lse is None:
         lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
     elif lse.shape != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous():
@@ -138,7 +152,13 @@ def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse
         stream = torch.cuda.current_stream(q.device)
     Hkv = k.shape[1]
     with torch.cuda.device(q.device):
-        if Hkv == H:
+        if dv != d:
+            if Hkv != H:
+                raise ValueError("unequal head dimensions need as many key/value heads as query heads")
+            status = qm_attn_fwd_mla(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                     lse.data_ptr(), B, H, N, d, dv, scale, 1 if causal else 0,
+                                     stream.cuda_stream, code)
+        elif Hkv == H:
             status = qm_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                                  lse.data_ptr(), B, H, N, d, scale, 1 if causal else 0,
                                  stream.cuda_stream, code)

@@ -162,6 +162,46 @@ struct Layout {
   static_assert(BUF % 16 == 0, "buffers stay 16-byte aligned");
 };
 
+// LDS layout of one K tile of DK columns: the first min(DK, 128) columns as a
+// Layout part, and (DK = 192) the remaining 64 columns as a second part right
+// after it.  Each part keeps whole rows per direct load.
+template <int DK>
+struct KTile {
+  static constexpr int W0 = DK < 128 ? DK : 128;  // columns of part 0
+  static constexpr int W1 = DK - W0;              // columns of part 1 (0 or 64)
+  using L0 = Layout<W0>;
+  using L1 = Layout<W1 ? W1 : 64>;                // unused when W1 == 0
+  static constexpr int NKS0 = W0 / 16;            // GEMM-I k-steps in part 0
+  static constexpr int OFF1 = L0::NG * L0::KGS;   // byte offset of part 1
+  static constexpr int BYTES = OFF1 + (W1 ? L1::NG * L1::KGS : 0);
+  static constexpr int GPW0 = L0::NG / kWaves;    // direct loads per wave, part 0
+  static constexpr int GPW1 = W1 ? L1::NG / kWaves : 0;
+  static constexpr int GPW = GPW0 + GPW1;         // direct loads per wave per K block
+  static_assert(W1 == 0 || W1 == 64, "K head dimensions 64, 128 and 192");
+};
+
+// Depth of the K and V rings: four 64-key blocks (one barrier per two blocks)
+// when four K and four V tiles fit the 160 KB of LDS, else two (one barrier
+// per block).
+template <int DK, int DV>
+constexpr int ring_depth() {
+  return 4 * (KTile<DK>::BYTES + Layout<DV>::VBYTES) <= 160 * 1024 ? 4 : 2;
+}
+
+template <int DK, int DV>
+constexpr size_t lds_bytes() {
+  return (size_t)ring_depth<DK, DV>() * (KTile<DK>::BYTES + Layout<DV>::VBYTES);
+}
+
+// Slot of exponential chunk c (of 16) in region 1 of NSLOT slots, and the
+// chunk placed in slot s (-1: none).
+__host__ __device__ constexpr int chunk_slot(int c, int nslot) { return c * nslot / 16; }
+__host__ __device__ constexpr int slot_chunk(int s, int nslot) {
+  for (int c = 0; c < 16; ++c)
+    if (chunk_slot(c, nslot) == s) return c;
+  return -1;
+}
+
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kRsrcWord3);
 }
@@ -215,12 +255,14 @@ __device__ __forceinline__ void lds_load16(i32x4 rs, uint32_t lds, uint32_t voff
                :: "v"(voff), "{m0}"(lds), "s"(rs) : "memory");
 }
 
-template <int D, int DT, bool CAUSAL>
+template <int DK, int DV, int DT, bool CAUSAL>
 __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
-  using L = Layout<D>;
-  constexpr int NKS = D / 16;          // GEMM-I k-steps
-  constexpr int NMT = D / 32;          // GEMM-II M tiles
-  constexpr int GPW = L::NG / kWaves;  // load groups per wave per tile
+  using KT = KTile<DK>;                  // K tile (DK columns)
+  using LV = Layout<DV>;                 // V tile (DV columns)
+  constexpr int NKS = DK / 16;           // GEMM-I k-steps
+  constexpr int NMT = DV / 32;           // GEMM-II M tiles
+  constexpr int GPWV = LV::NG / kWaves;  // V direct loads per wave per block
+  constexpr int RING = ring_depth<DK, DV>();
 
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   char* const lds = reinterpret_cast<char*>(smem);
@@ -252,12 +294,11 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
   // workgroups run on one XCD and share its L2 for the K/V stream.
   const int b = bh / p.H;
   const int bhkv = b * p.Hkv + (bh - b * p.H) / p.group;
-  const size_t head = (size_t)bh * (size_t)N * D;
-  const size_t head_kv = (size_t)bhkv * (size_t)N * D;
-  const uint32_t head_bytes = (uint32_t)N * D * 2;
-  const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + head, head_bytes);
-  const i32x4 rk = make_dma_rsrc(p.k + head_kv, head_bytes);
-  const i32x4 rv = make_dma_rsrc(p.v + head_kv, head_bytes);
+  const uint32_t head_bytes_k = (uint32_t)N * DK * 2;   // one head of q or k
+  const uint32_t head_bytes_v = (uint32_t)N * DV * 2;   // one head of v or o
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + (size_t)bh * N * DK, head_bytes_k);
+  const i32x4 rk = make_dma_rsrc(p.k + (size_t)bhkv * N * DK, head_bytes_k);
+  const i32x4 rv = make_dma_rsrc(p.v + (size_t)bhkv * N * DV, head_bytes_v);
   // zero-size descriptors: a load through one touches no memory and writes zeros
   const i32x4 rk0 = i32x4{rk[0], rk[1], 0, rk[3]};
   const i32x4 rv0 = i32x4{rv[0], rv[1], 0, rv[3]};
@@ -271,7 +312,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     u32x4 qf[NKS];
   #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
-      qf[ks] = __builtin_amdgcn_raw_buffer_load_b128(rq, (uint32_t)(qrow * D + 16 * ks + 8 * hi) * 2, 0, 0);
+      qf[ks] = __builtin_amdgcn_raw_buffer_load_b128(rq, (uint32_t)(qrow * DK + 16 * ks + 8 * hi) * 2, 0, 0);
       if (p.qmode == kQNegate) qf[ks] ^= 0x80008000u;
       if (p.qmode == kQZero) qf[ks] = u32x4{0, 0, 0, 0};
     }
@@ -286,69 +327,97 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     float l_run = 0.f;         // this lane's share of the running row sum
 
     // ---- HBM -> LDS: this wave's load groups of one K or V block ----
-    // LDS: four K slots, then four V slots, of one 64-key block each
-    constexpr int VOFF = 4 * L::KBYTES;
-    // lane part of the global offset (row slot, 16-byte unit), plus the row of
-    // the load group
-    const uint32_t load_lane_off = (uint32_t)(L::NG * (lane / L::U) * D * 2 + (lane % L::U) * 16);
+    // LDS: RING K slots, then RING V slots, of one 64-key block each
+    constexpr int VOFF = RING * KT::BYTES;
+    // lane parts of the global offsets (row slot, 16-byte unit, column of the
+    // K part); the row of the load group is added per load
+    const uint32_t koff0 = (uint32_t)(KT::L0::NG * (lane / KT::L0::U) * DK * 2 + (lane % KT::L0::U) * 16);
+    const uint32_t koff1 = (uint32_t)(KT::L1::NG * (lane / KT::L1::U) * DK * 2 + KT::W0 * 2 +
+                                      (lane % KT::L1::U) * 16);
+    const uint32_t voff = (uint32_t)(LV::NG * (lane / LV::U) * DV * 2 + (lane % LV::U) * 16);
     auto lds_addr = [&](int byte_off) { return (uint32_t)(uintptr_t)(lds_void*)(lds + byte_off); };
-    auto load_k = [&](int j0, int kb) {
-  #pragma unroll
-      for (int i = 0; i < GPW; ++i) {
-        const int g = wave * GPW + i;
-        lds_load16(rk, lds_addr(kb * L::KBYTES + g * L::KGS), load_lane_off + (uint32_t)((j0 + g) * D) * 2);
+    // load i (of KT::GPW) of this wave for K block blk into K slot kb
+    auto k_load = [&](int i, int blk, int kb, i32x4 rs) __attribute__((always_inline)) {
+      if (i < KT::GPW0) {
+        const int g = wave * KT::GPW0 + i;
+        lds_load16(rs, lds_addr(kb * KT::BYTES + g * KT::L0::KGS),
+                   koff0 + (uint32_t)((blk * kBN + g) * DK) * 2);
+      } else {
+        const int g = wave * KT::GPW1 + (i - KT::GPW0);
+        lds_load16(rs, lds_addr(kb * KT::BYTES + KT::OFF1 + g * KT::L1::KGS),
+                   koff1 + (uint32_t)((blk * kBN + g) * DK) * 2);
       }
     };
-    auto load_v = [&](int j0, int vb) {
+    // load i (of GPWV) of this wave for V block blk into V slot vb
+    auto v_load = [&](int i, int blk, int vb, i32x4 rs) __attribute__((always_inline)) {
+      const int g = wave * GPWV + i;
+      lds_load16(rs, lds_addr(VOFF + vb * LV::VBYTES + g * LV::VGS),
+                 voff + (uint32_t)((blk * kBN + g) * DV) * 2);
+    };
+    auto load_k = [&](int blk, int kb) {
   #pragma unroll
-      for (int i = 0; i < GPW; ++i) {
-        const int g = wave * GPW + i;
-        lds_load16(rv, lds_addr(VOFF + vb * L::VBYTES + g * L::VGS),
-                   load_lane_off + (uint32_t)((j0 + g) * D) * 2);
-      }
+      for (int i = 0; i < KT::GPW; ++i) k_load(i, blk, kb, rk);
+    };
+    auto load_v = [&](int blk, int vb) {
+  #pragma unroll
+      for (int i = 0; i < GPWV; ++i) v_load(i, blk, vb, rv);
     };
 
-    // Direct load n (of 2 GPW) issued during block j, Q = j % 4: an even block
-    // loads K(j+3) and K(j+4) into K slots (Q+3) % 4 and Q, an odd block V(j+1)
-    // and V(j+2) into V slots (Q+1) % 4 and (Q+2) % 4, GPW groups each.  Loads of
-    // blocks past the last go through the zero-size descriptor (into slots no
-    // one reads again).
+    // Direct loads issued during block j, Q = j % 4 (loads of blocks past the
+    // last go through the zero-size descriptor, into slots no one reads again).
+    //   RING = 4: an even block loads K(j+3) and K(j+4) into K slots (Q+3) % 4
+    //             and Q, an odd block V(j+1) and V(j+2) into V slots (Q+1) % 4
+    //             and (Q+2) % 4;
+    //   RING = 2: every block loads K(j+2) into K slot Q % 2 and V(j+1) into V
+    //             slot (Q+1) % 2.
+    auto n_dma = [](auto ph) {
+      constexpr int Q = decltype(ph)::value;
+      return RING == 4 ? (Q % 2 == 0 ? 2 * KT::GPW : 2 * GPWV) : KT::GPW + GPWV;
+    };
     auto dma = [&](auto ph, int n, int j) __attribute__((always_inline)) {
       constexpr int Q = decltype(ph)::value;
-      const int second = n >= GPW ? 1 : 0;
-      const int g = wave * GPW + (n - second * GPW);
-      if (Q % 2 == 0) {
+      if (RING == 4 && Q % 2 == 0) {
+        const int second = n >= KT::GPW ? 1 : 0;
         const int blk = j + 3 + second;
-        lds_load16(blk < nkv ? rk : rk0, lds_addr(((Q + 3 + second) % 4) * L::KBYTES + g * L::KGS),
-                   load_lane_off + (uint32_t)((blk * kBN + g) * D) * 2);
-      } else {
+        k_load(n - second * KT::GPW, blk, (Q + 3 + second) % 4, blk < nkv ? rk : rk0);
+      } else if (RING == 4) {
+        const int second = n >= GPWV ? 1 : 0;
         const int blk = j + 1 + second;
-        lds_load16(blk < nkv ? rv : rv0,
-                   lds_addr(VOFF + ((Q + 1 + second) % 4) * L::VBYTES + g * L::VGS),
-                   load_lane_off + (uint32_t)((blk * kBN + g) * D) * 2);
+        v_load(n - second * GPWV, blk, (Q + 1 + second) % 4, blk < nkv ? rv : rv0);
+      } else if (n < KT::GPW) {
+        k_load(n, j + 2, Q % 2, j + 2 < nkv ? rk : rk0);
+      } else {
+        v_load(n - KT::GPW, j + 1, (Q + 1) % 2, j + 1 < nkv ? rv : rv0);
       }
     };
 
     // per-lane LDS byte bases of the operand reads; every read adds a constant
-    //   K (A of GEMM-I): row r = 32 kt + l32 -> group r % NG, slot r / NG; unit 2 ks + hi
-    const int k_base = (l32 % L::NG) * L::KGS + (l32 / L::NG) * L::ROW + 16 * hi;
+    //   K (A of GEMM-I): row r = 32 kt + l32 -> group r % NG, slot r / NG of
+    //   its part; unit 2 ks + hi
+    const int k_base0 = (l32 % KT::L0::NG) * KT::L0::KGS + (l32 / KT::L0::NG) * KT::L0::ROW + 16 * hi;
+    const int k_base1 = KT::OFF1 + (l32 % KT::L1::NG) * KT::L1::KGS +
+                        (l32 / KT::L1::NG) * KT::L1::ROW + 16 * hi;
     //   V (A of GEMM-II, transposing read): key = 16 u + 8 h2 + kq, dims d0 .. d0+3
     const int grp = lane >> 4;
     const int sl = lane & 15;
     const int kq = 4 * (grp >> 1) + (sl >> 2);
-    const int v_base = VOFF + kq * L::VGS + 2 * (16 * (grp & 1) + 4 * (sl & 3));
+    const int v_base = VOFF + kq * LV::VGS + 2 * (16 * (grp & 1) + 4 * (sl & 3));
 
     auto k_read = [&](int kb, int kt, int ks) {
-      constexpr int SLOTS_PER_32 = 32 / L::NG;
-      return *reinterpret_cast<const u32x4*>(lds + kb * L::KBYTES + k_base +
-                                             kt * SLOTS_PER_32 * L::ROW + 32 * ks);
+      if (ks < KT::NKS0) {
+        return *reinterpret_cast<const u32x4*>(lds + kb * KT::BYTES + k_base0 +
+                                               kt * (32 / KT::L0::NG) * KT::L0::ROW + 32 * ks);
+      }
+      return *reinterpret_cast<const u32x4*>(lds + kb * KT::BYTES + k_base1 +
+                                             kt * (32 / KT::L1::NG) * KT::L1::ROW +
+                                             32 * (ks - KT::NKS0));
     };
     auto v_read = [&](int vb, int mt, int u, int h2) {
       // group of key 16 u + 8 h2 + kq is (16 u + 8 h2) % NG + kq, slot (16 u + 8 h2) / NG
-      const int g_off = (16 * u + 8 * h2) % L::NG;
-      const int slot = (16 * u + 8 * h2) / L::NG;
+      const int g_off = (16 * u + 8 * h2) % LV::NG;
+      const int slot = (16 * u + 8 * h2) / LV::NG;
       return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (lds_i16x4*)(lds + vb * L::VBYTES + v_base + g_off * L::VGS + slot * L::ROW + 64 * mt));
+          (lds_i16x4*)(lds + vb * LV::VBYTES + v_base + g_off * LV::VGS + slot * LV::ROW + 64 * mt));
     };
 
     // whether this wave has a visible key in block j (causal: blocks above its rows are skipped)
@@ -390,9 +459,11 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
         __attribute__((always_inline)) {
       const int j0 = j * kBN;
       constexpr int AHEAD = 4;
-      constexpr int NG1 = 2 * NKS;        // GEMM-I MFMAs per block
-      constexpr int STRIDE = 16 / NG1;    // exponential chunks per GEMM-I MFMA
-      constexpr int NV = 4 * NMT;         // GEMM-II MFMAs per block
+      constexpr int NG1 = 2 * NKS;                    // GEMM-I MFMAs per block
+      constexpr int NSLOT = NG1 > 16 ? NG1 : 16;      // slots of region 1
+      constexpr int NV = 4 * NMT;                     // GEMM-II MFMAs per block
+      constexpr int NDMA = n_dma(decltype(ph){});     // direct loads in this block
+      constexpr int DSTRIDE = (NSLOT / 2) / NDMA > 0 ? (NSLOT / 2) / NDMA : 1;
       // first K fragments of GEMM-I for block j+1: their LDS latency runs under
       // the mask work below
       u32x4 kring[AHEAD];
@@ -439,9 +510,10 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
         lsum += e0 + e1;
       };
 
-      // Straight-line region 1, written as 16 slots that each issue the next
-      // MFMA of GEMM-I for block j+1 (every slot at d = 128, every other slot at
-      // d = 64) and advance the exponentials of block j through a three-stage
+      // Straight-line region 1, written as NSLOT slots (16, or 24 when GEMM-I
+      // has 24 MFMAs at DK = 192).  The slots issue the MFMAs of GEMM-I for
+      // block j+1 (every slot at DK = 128 and 192, every other slot at 64) and
+      // advance the 16 exponential chunks of block j through a three-stage
       // software pipeline: the FMAs of pair i+2, the exponentials of pair i+1,
       // and the pack and row-sum adds of pair i, so that no instruction waits
       // on a result produced in its own slot.  Operand reads run AHEAD MFMAs
@@ -467,16 +539,21 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
       ea[0] = __builtin_amdgcn_exp2f(xa[0]);
       eb[0] = __builtin_amdgcn_exp2f(xb[0]);
   #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        if (i % STRIDE == 0) {
-          const int m = i / STRIDE;       // MFMA m: k-step m / 2, key tile m % 2
+      for (int sidx = 0; sidx < NSLOT; ++sidx) {
+        if ((sidx * NG1) % NSLOT == 0) {
+          const int m = sidx * NG1 / NSLOT;   // MFMA m: k-step m / 2, key tile m % 2
           const u32x4 a = kring[m % AHEAD];
           if (m + AHEAD < NG1) kring[m % AHEAD] = k_read(kb_next, (m + AHEAD) % 2, (m + AHEAD) / 2);
           s_next[m % 2] = Half<DT>::mfma(a, qf[m / 2], s_next[m % 2]);
         }
-        if (i >= 16 - AHEAD) vring[i - (16 - AHEAD)] = v_frag(i - (16 - AHEAD));
+        if (sidx >= NSLOT - AHEAD) vring[sidx - (NSLOT - AHEAD)] = v_frag(sidx - (NSLOT - AHEAD));
         // this block's direct loads, spread over the first half of the region
-        if (i % (8 / (2 * GPW)) == 0 && i / (8 / (2 * GPW)) < 2 * GPW) dma(ph, i / (8 / (2 * GPW)), j);
+        if (sidx % DSTRIDE == 0 && sidx / DSTRIDE < NDMA) dma(ph, sidx / DSTRIDE, j);
+        const int i = slot_chunk(sidx, NSLOT);
+        if (i < 0) {
+          __builtin_amdgcn_sched_barrier(0);
+          continue;
+        }
         if (i + 1 < 16) {
           ea[i + 1] = __builtin_amdgcn_exp2f(xa[i + 1]);
           eb[i + 1] = __builtin_amdgcn_exp2f(xb[i + 1]);
@@ -527,14 +604,15 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
       }
     };
 
-    // Pipeline.  Block j (Q = j % 4) finds K(j+1) in K slot (Q+1) % 4 and V(j)
-    // in V slot Q, and issues the direct loads of the pair of blocks after the
-    // next (see dma above).  One barrier per pair of blocks, after each odd
-    // block: it publishes the pair's loads (each wave first waits for its own)
-    // and retires the pair's reads of the slots the next pair refills.  So
-    // the rings hold four blocks: two being read, two being loaded.  Blocks a
-    // wave skips (causal) come only after all the blocks it computes; it still
-    // issues their loads.
+    // Pipeline.  Block j (Q = j % 4) finds K(j+1) in K slot (Q+1) % RING and
+    // V(j) in V slot Q % RING, and issues direct loads (see dma above).
+    // RING = 4: one barrier per pair of blocks, after each odd block: it
+    // publishes the pair's loads (each wave first waits for its own) and
+    // retires the pair's reads of the slots the next pair refills, so the
+    // rings hold two blocks being read and two being loaded.  RING = 2: one
+    // barrier per block, one block read and one loaded.  Blocks a wave skips
+    // (causal) come only after all the blocks it computes; it still issues
+    // their loads.
     f32x16 sa[2], sb[2];
     auto sync = [&]() __attribute__((always_inline)) {
       __builtin_amdgcn_s_waitcnt(kWaitLoads);
@@ -544,19 +622,19 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
         __attribute__((always_inline)) {
       constexpr int Q = decltype(ph)::value;
       if (active(j)) {
-        block(ph, j, (Q + 1) % 4, Q, s_cur, s_next);
+        block(ph, j, (Q + 1) % RING, Q % RING, s_cur, s_next);
       } else {
   #pragma unroll
-        for (int n = 0; n < 2 * GPW; ++n) dma(ph, n, j);
+        for (int n = 0; n < n_dma(ph); ++n) dma(ph, n, j);
       }
-      if (Q % 2 == 1) sync();
+      if (RING == 2 || Q % 2 == 1) sync();
     };
 
     load_k(0, 0);
     load_v(0, 0);
-    if (nkv > 1) load_k(kBN, 1);
-    if (nkv > 2) load_k(2 * kBN, 2);
-    if (nkv > 1) load_v(kBN, 1);
+    if (nkv > 1) load_k(1, 1);
+    if (RING == 4 && nkv > 2) load_k(2, 2);
+    if (RING == 4 && nkv > 1) load_v(1, 1);
     __builtin_amdgcn_s_waitcnt(kWaitLoads);
     __syncthreads();
     if (active(0)) gemm1(0, sa);
@@ -577,19 +655,19 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     }
     // a lone last block still ends with a barrier (kept out of the loop: a
     // barrier on a loop exit path makes the register allocator spill)
-    if (nkv % 2 == 1) sync();
+    if (RING == 4 && nkv % 2 == 1) sync();
 
     // ---- epilogue: O = O / l in the storage type, lse in natural log ----
     const float l_tot = sum_across_halves(l_run);
     const float inv = 1.0f / l_tot;
-    const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.o + head, head_bytes);
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.o + (size_t)bh * N * DV, head_bytes_v);
   #pragma unroll
     for (int mt = 0; mt < NMT; ++mt) {
   #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const u32x2 w = {Half<DT>::pack(oacc[mt][4 * g] * inv, oacc[mt][4 * g + 1] * inv),
                          Half<DT>::pack(oacc[mt][4 * g + 2] * inv, oacc[mt][4 * g + 3] * inv)};
-        __builtin_amdgcn_raw_buffer_store_b64(w, ro, (uint32_t)(qrow * D + 32 * mt + 8 * g + 4 * hi) * 2, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b64(w, ro, (uint32_t)(qrow * DV + 32 * mt + 8 * g + 4 * hi) * 2, 0, 0);
       }
     }
     if (hi == 0) {
@@ -602,15 +680,11 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
   if (CAUSAL && qbs[1] >= 0) run(qbs[1]);
 }
 
-template <int D>
-constexpr size_t lds_bytes() {
-  return 4 * (size_t)(Layout<D>::KBYTES + Layout<D>::VBYTES);
-}
-
-template <int D, int DT, bool CAUSAL>
+template <int DK, int DV, int DT, bool CAUSAL>
 hipError_t launch_instance(const KParams& kp, hipStream_t stream) {
-  auto kern = attn_fwd_kernel<D, DT, CAUSAL>;
-  constexpr size_t lds = lds_bytes<D>();
+  auto kern = attn_fwd_kernel<DK, DV, DT, CAUSAL>;
+  constexpr size_t lds = lds_bytes<DK, DV>();
+  static_assert(lds <= 160 * 1024, "one workgroup's LDS fits a CU");
   static const hipError_t attr = hipFuncSetAttribute(
       reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (attr != hipSuccess) return attr;
@@ -636,16 +710,22 @@ hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
   kp.total = kp.wg_per_head * a.B * a.H;
   kp.c = a.c;
   kp.qmode = a.qmode;
-  const int key = (a.d == 128 ? 4 : 0) | (a.dtype << 1) | a.causal;
+  // head dimensions (d_qk, d_v): 64/64, 128/128, 192/128
+  const int dims = a.d == 64 ? 0 : (a.d == 128 ? 1 : 2);
+  const int key = dims * 4 + a.dtype * 2 + a.causal;
   switch (key) {
-    case 0: return launch_instance<64, 0, false>(kp, stream);
-    case 1: return launch_instance<64, 0, true>(kp, stream);
-    case 2: return launch_instance<64, 1, false>(kp, stream);
-    case 3: return launch_instance<64, 1, true>(kp, stream);
-    case 4: return launch_instance<128, 0, false>(kp, stream);
-    case 5: return launch_instance<128, 0, true>(kp, stream);
-    case 6: return launch_instance<128, 1, false>(kp, stream);
-    case 7: return launch_instance<128, 1, true>(kp, stream);
+    case 0: return launch_instance<64, 64, 0, false>(kp, stream);
+    case 1: return launch_instance<64, 64, 0, true>(kp, stream);
+    case 2: return launch_instance<64, 64, 1, false>(kp, stream);
+    case 3: return launch_instance<64, 64, 1, true>(kp, stream);
+    case 4: return launch_instance<128, 128, 0, false>(kp, stream);
+    case 5: return launch_instance<128, 128, 0, true>(kp, stream);
+    case 6: return launch_instance<128, 128, 1, false>(kp, stream);
+    case 7: return launch_instance<128, 128, 1, true>(kp, stream);
+    case 8: return launch_instance<192, 128, 0, false>(kp, stream);
+    case 9: return launch_instance<192, 128, 0, true>(kp, stream);
+    case 10: return launch_instance<192, 128, 1, false>(kp, stream);
+    case 11: return launch_instance<192, 128, 1, true>(kp, stream);
   }
   return hipErrorInvalidValue;
 }

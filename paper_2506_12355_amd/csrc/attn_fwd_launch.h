@@ -22,7 +22,8 @@ struct AttnArgs {
   const uint16_t* v;
   uint16_t* o;
   float* lse;
-  int B, H, N, d;
+  int B, H, N, d;  // d: head dimension of q and k (d_qk)
+  int dv;         // head dimension of v and o: d, or 128 when d = 192
   int Hkv;      // key/value heads; H % Hkv == 0, query head h reads h / (H / Hkv)
   int causal;   // 0 or 1
   int dtype;    // 0 = fp16, 1 = bf16
@@ -30,7 +31,7 @@ struct AttnArgs {
   int qmode;    // QMode
 };
 
-// Enqueues the kernel instance for (d, dtype, causal).  Arguments have been
+// Enqueues the kernel instance for (d, dv, dtype, causal).  Arguments have been
 // validated by the caller.  Returns the HIP launch status.
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream);
 

@@ -28,18 +28,22 @@ bool finite_bits(float x) {
   return (u & 0x7F800000u) != 0x7F800000u;
 }
 
-// Validation and dispatch shared by both entry points: H query heads read Hkv
-// key/value heads (Hkv == H for plain multi-head attention).
+// Validation and dispatch shared by the entry points: H query heads read Hkv
+// key/value heads (Hkv == H for plain multi-head attention); q and k have head
+// dimension d, v and o head dimension dv.
 int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H,
-             int Hkv, int N, int d, float scale, int causal, hipStream_t stream, int dtype) {
+             int Hkv, int N, int d, int dv, float scale, int causal, hipStream_t stream,
+             int dtype) {
   if (!q || !k || !v || !o || !lse) return QM_ERR_NULL;
   if (B < 1 || H < 1 || N < 1 || Hkv < 1 || Hkv > H || H % Hkv != 0) return QM_ERR_SHAPE;
-  if (d != 64 && d != 128) return QM_ERR_HEADDIM;
+  if (!((d == 64 && dv == 64) || (d == 128 && dv == 128) || (d == 192 && dv == 128)))
+    return QM_ERR_HEADDIM;
   // element counts: the whole tensor in 62 bits, one head's [N][d] slab and the
   // workgroup count in 31 bits (the kernels index within a head in 32 bits)
   const uint64_t bh = (uint64_t)B * (uint64_t)H;
   const uint64_t bhkv = (uint64_t)B * (uint64_t)Hkv;
-  const uint64_t nd = (uint64_t)N * (uint64_t)d;
+  const uint64_t nd = (uint64_t)N * (uint64_t)d;     // d >= dv
+  const uint64_t ndv = (uint64_t)N * (uint64_t)dv;
   // a head's byte offsets, including the padded last 256-row query block, fit
   // in 32 bits; the workgroup count fits an int
   if ((uint64_t)(N + 256) * (uint64_t)d >= (1ull << 31) || bh >= (1ull << 62) / nd)
@@ -50,12 +54,14 @@ int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, i
   if (causal != 0 && causal != 1) return QM_ERR_CAUSAL;
 
   const size_t q_bytes = (size_t)(bh * nd) * 2;
-  const size_t kv_bytes = (size_t)(bhkv * nd) * 2;
+  const size_t k_bytes = (size_t)(bhkv * nd) * 2;
+  const size_t v_bytes = (size_t)(bhkv * ndv) * 2;
+  const size_t o_bytes = (size_t)(bh * ndv) * 2;
   const size_t lse_bytes = (size_t)(bh * (uint64_t)N) * sizeof(float);
-  if (overlaps(o, q_bytes, q, q_bytes) || overlaps(o, q_bytes, k, kv_bytes) ||
-      overlaps(o, q_bytes, v, kv_bytes) || overlaps(lse, lse_bytes, q, q_bytes) ||
-      overlaps(lse, lse_bytes, k, kv_bytes) || overlaps(lse, lse_bytes, v, kv_bytes) ||
-      overlaps(lse, lse_bytes, o, q_bytes))
+  if (overlaps(o, o_bytes, q, q_bytes) || overlaps(o, o_bytes, k, k_bytes) ||
+      overlaps(o, o_bytes, v, v_bytes) || overlaps(lse, lse_bytes, q, q_bytes) ||
+      overlaps(lse, lse_bytes, k, k_bytes) || overlaps(lse, lse_bytes, v, v_bytes) ||
+      overlaps(lse, lse_bytes, o, o_bytes))
     return QM_ERR_ALIAS;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse))
     return QM_ERR_UNSUPPORTED;
@@ -71,6 +77,7 @@ int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, i
   a.Hkv = Hkv;
   a.N = N;
   a.d = d;
+  a.dv = dv;
   a.causal = causal;
   a.dtype = dtype;
   // exp2-domain scale; the sign goes into Q (exact), a zero or negligible
@@ -91,13 +98,19 @@ int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, i
 extern "C" int qm_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
                            int B, int H, int N, int d, float scale, int causal,
                            hipStream_t stream, int dtype) {
-  return attn_fwd(q, k, v, o, lse, B, H, H, N, d, scale, causal, stream, dtype);
+  return attn_fwd(q, k, v, o, lse, B, H, H, N, d, d, scale, causal, stream, dtype);
 }
 
 extern "C" int qm_attn_fwd_gqa(const void* q, const void* k, const void* v, void* o,
                                float* lse, int B, int H, int Hkv, int N, int d, float scale,
                                int causal, hipStream_t stream, int dtype) {
-  return attn_fwd(q, k, v, o, lse, B, H, Hkv, N, d, scale, causal, stream, dtype);
+  return attn_fwd(q, k, v, o, lse, B, H, Hkv, N, d, d, scale, causal, stream, dtype);
+}
+
+extern "C" int qm_attn_fwd_mla(const void* q, const void* k, const void* v, void* o,
+                               float* lse, int B, int H, int N, int d_qk, int d_v, float scale,
+                               int causal, hipStream_t stream, int dtype) {
+  return attn_fwd(q, k, v, o, lse, B, H, H, N, d_qk, d_v, scale, causal, stream, dtype);
 }
 
 extern "C" const char* qm_attn_strerror(int status) {
@@ -106,7 +119,8 @@ extern "C" const char* qm_attn_strerror(int status) {
     case QM_ERR_NULL: return "a tensor pointer is NULL";
     case QM_ERR_SHAPE:
       return "B, H or N is below 1, Hkv does not divide H, or the tensors are too large";
-    case QM_ERR_HEADDIM: return "head dimension d must be 64 or 128";
+    case QM_ERR_HEADDIM:
+      return "head dimensions must be 64 or 128 (or d_qk = 192 with d_v = 128)";
     case QM_ERR_DTYPE: return "dtype must be QM_F16 (0) or QM_BF16 (1)";
     case QM_ERR_SCALE: return "scale must be finite";
     case QM_ERR_ALIAS: return "o or lse overlaps an input or each other";

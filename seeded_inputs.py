@@ -11,7 +11,8 @@ stand in for its long-context workloads of the Evaluation section's
 * ``rng = numpy.random.default_rng(seed)`` (PCG64), seed 0 unless stated;
 * draw ``standard_normal(shape, float32)`` for Q, then K, then V; Q has shape
   ``[B, H, N, d]`` and K, V ``[B, Hkv, N, d]`` (Hkv = H unless a grouped-query
-  workload names fewer key/value heads);
+  workload names fewer key/value heads; V's last dimension is d_v when a
+  workload gives values their own head dimension);
 * optionally multiply Q and K by an exact power of two in fp32 (the sharper
   long-context workload uses 2);
 * round to fp16 (numpy's cast, round-to-nearest-even) or to bf16 with
@@ -50,19 +51,21 @@ def round_to_storage(x: np.ndarray, dtype: str) -> np.ndarray:
 
 
 def make_qkv(B: int, H: int, N: int, d: int, dtype: str, seed: int = 0,
-             qk_mult: float = 1.0, Hkv: int | None = None):
-    """Draw Q [B, H, N, d] and K, V [B, Hkv, N, d] and round them to ``dtype``.
+             qk_mult: float = 1.0, Hkv: int | None = None, dv: int | None = None):
+    """Draw Q [B, H, N, d], K [B, Hkv, N, d] and V [B, Hkv, N, dv], rounded to
+    ``dtype``.
 
-    ``Hkv`` defaults to H.  Returns three contiguous arrays (``float16`` or
-    bf16 ``uint16`` bits).
+    ``Hkv`` defaults to H and ``dv`` to d.  Returns three contiguous arrays
+    (``float16`` or bf16 ``uint16`` bits).
     """
     if dtype not in DTYPES:
         raise ValueError(f"unknown dtype {dtype!r}")
     Hkv = H if Hkv is None else Hkv
+    dv = d if dv is None else dv
     rng = np.random.default_rng(seed)
     out = []
     for name in ("q", "k", "v"):
-        shape = (B, H, N, d) if name == "q" else (B, Hkv, N, d)
+        shape = {"q": (B, H, N, d), "k": (B, Hkv, N, d), "v": (B, Hkv, N, dv)}[name]
         x = rng.standard_normal(shape, dtype=np.float32)
         if name in ("q", "k") and qk_mult != 1.0:
             x *= np.float32(qk_mult)
@@ -89,18 +92,23 @@ class Workload:
     qk_mult: float = 1.0
     seed: int = 0
     Hkv: int = 0          # key/value heads; 0 means H (multi-head attention)
+    dv: int = 0           # head dimension of V and O; 0 means d
 
     @property
     def kv_heads(self) -> int:
         return self.Hkv or self.H
 
     @property
+    def d_v(self) -> int:
+        return self.dv or self.d
+
+    @property
     def scale(self) -> float:
-        return default_scale(self.d)
+        return default_scale(self.d)   # 1/sqrt of the query/key head dimension
 
     def inputs(self):
         return make_qkv(self.B, self.H, self.N, self.d, self.dtype,
-                        seed=self.seed, qk_mult=self.qk_mult, Hkv=self.kv_heads)
+                        seed=self.seed, qk_mult=self.qk_mult, Hkv=self.kv_heads, dv=self.d_v)
 
 
 WORKLOADS = {
@@ -122,6 +130,15 @@ WORKLOADS = {
                  Hkv=1),
         Workload("gqa_b2_h8_kv2_n1000_d64_f16", 2, 8, 1000, 64, "f16", (False, True), Hkv=2),
         Workload("mqa_b2_h6_kv1_n777_d128_bf16", 2, 6, 777, 128, "bf16", (False, True), Hkv=1),
+        # the MLA shape in explicit form: head dimension 128 plus a 64-wide RoPE
+        # part for queries and keys (d = 192), values and outputs 128 wide, with
+        # DeepSeek-V3's 128 heads at the 16k-token budget, causal (the paper's
+        # MLA table), plus smaller cases
+        Workload("mla_b2_h128_n8192_d192_dv128_bf16_causal", 2, 128, 8192, 192, "bf16",
+                 (True,), dv=128),
+        Workload("mla_b1_h16_n4096_d192_dv128_bf16", 1, 16, 4096, 192, "bf16",
+                 (False, True), dv=128),
+        Workload("mla_b2_h4_n777_d192_dv128_f16", 2, 4, 777, 192, "f16", (False, True), dv=128),
     )
 }
 

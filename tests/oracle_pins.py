@@ -14,7 +14,9 @@ acceleration") fixes independently of any implementation:
   sharp one-hot row, large scales without overflow);
 * grouped-query attention: each query head against the brute force with its
   group's key/value head, equality with explicitly repeated key/value heads,
-  identical query heads under multi-query attention.
+  identical query heads under multi-query attention;
+* values narrower than queries and keys (the MLA shape): the brute force, and
+  output columns that depend only on their own value column.
 
 ``tests/test_oracle.py`` runs every pin on the oracle and shows that planted
 mistakes in the oracle fail at least one pin.
@@ -367,6 +369,48 @@ def pin_mqa_identical_query_heads(mod):
             _close(lse[0, h], l1[0, 0], 0.0, "MQA identical heads lse")
 
 
+MLA_BRUTE_CASES = [
+    # (N, d, dv, dtype, scale, causal, seed): wider queries/keys than values
+    (5, 12, 8, "f16", 0.3, True, 51),
+    (6, 24, 16, "bf16", 1.0 / math.sqrt(24), False, 52),
+    (4, 8, 4, "bf16", -0.6, True, 53),
+]
+
+
+def pin_mla_brute_force(mod):
+    """Values narrower than queries and keys (the MLA shape): scores over all d
+    columns, outputs with dv columns, against the 50-digit brute force."""
+    for N, d, dv, dtype, scale, causal, seed in MLA_BRUTE_CASES:
+        q, k, v = make_qkv(1, 2, N, d, dtype, seed=seed, dv=dv)
+        O, lse = mod.attention_fp64(q, k, v, scale, causal, dtype, row_block=2)
+        if O.shape != (1, 2, N, dv):
+            raise AssertionError(f"MLA output shape {O.shape}")
+        s32 = float(np.float32(scale))
+        for h in range(2):
+            qf = _decode_independent(q[0, h], dtype)
+            kf = _decode_independent(k[0, h], dtype)
+            vf = _decode_independent(v[0, h], dtype)
+            Ob, lb = brute_force_decimal(qf, kf, vf, s32, causal)
+            tol = 1e-13 * (1.0 + abs(s32) * float(np.max(np.abs(qf @ kf.T))))
+            _close(O[0, h], Ob, tol * max(1.0, float(np.max(np.abs(vf)))), f"MLA O d={d} dv={dv}")
+            _close(lse[0, h], lb, tol * max(1.0, float(np.max(np.abs(lb)))), f"MLA lse d={d} dv={dv}")
+
+
+def pin_value_columns_independent(mod):
+    """Each output column depends only on the same column of V: splitting V's
+    columns into two halves and attending twice gives the two halves of O, and
+    lse does not depend on V at all."""
+    q, k, v = make_qkv(2, 3, 19, 12, "f16", seed=54, dv=10)
+    for causal in (False, True):
+        O, lse = mod.attention_fp64(q, k, v, 0.4, causal, "f16", row_block=7)
+        O1, l1 = mod.attention_fp64(q, k, np.ascontiguousarray(v[..., :4]), 0.4, causal, "f16")
+        O2, l2 = mod.attention_fp64(q, k, np.ascontiguousarray(v[..., 4:]), 0.4, causal, "f16")
+        _close(O[..., :4], O1, 1e-14, "V columns 0..3")
+        _close(O[..., 4:], O2, 1e-14, "V columns 4..9")
+        _close(l1, lse, 0.0, "lse independent of V")
+        _close(l2, lse, 0.0, "lse independent of V")
+
+
 ALL_PINS = [
     pin_brute_force,
     pin_zero_query_mean,
@@ -384,4 +428,6 @@ ALL_PINS = [
     pin_gqa_brute_force,
     pin_gqa_is_mha_on_repeated_heads,
     pin_mqa_identical_query_heads,
+    pin_mla_brute_force,
+    pin_value_columns_independent,
 ]

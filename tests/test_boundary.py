@@ -37,7 +37,8 @@ def _declared_functions():
 
 
 def test_header_declares_entry_points():
-    assert {"qm_attn_fwd", "qm_attn_fwd_gqa", "qm_attn_strerror"} <= set(_declared_functions())
+    assert {"qm_attn_fwd", "qm_attn_fwd_gqa", "qm_attn_fwd_mla",
+            "qm_attn_strerror"} <= set(_declared_functions())
 
 
 def test_library_exports_every_declared_symbol(lib):
@@ -139,6 +140,38 @@ def test_gqa_alias_extent_follows_kv_heads(lib):
     kv_bytes = 1 * 2 * 128 * 64 * 2          # B=1, Hkv=2, N=128, d=64, 16-bit
     assert call_gqa(2, H=8, o=K + kv_bytes, lse=L + 4) == qa.QM_ERR_UNSUPPORTED
     assert call_gqa(8, H=8, o=K + kv_bytes, lse=L + 4) == qa.QM_ERR_ALIAS
+
+
+def call_mla(d_qk, d_v, **over):
+    a = dict(GOOD)
+    a.update(over)
+    return qa.qm_attn_fwd_mla(a["q"], a["k"], a["v"], a["o"], a["lse"], a["B"], a["H"], a["N"],
+                              d_qk, d_v, a["scale"], a["causal"], a["stream"], a["dtype"])
+
+
+@pytest.mark.parametrize("d_qk,d_v,over,status", [
+    (192, 192, {}, qa.QM_ERR_HEADDIM),
+    (128, 64, {}, qa.QM_ERR_HEADDIM),
+    (192, 64, {}, qa.QM_ERR_HEADDIM),
+    (256, 128, {}, qa.QM_ERR_HEADDIM),
+    (64, 128, {}, qa.QM_ERR_HEADDIM),
+    (192, 128, dict(v=None), qa.QM_ERR_NULL),
+    (192, 128, dict(N=0), qa.QM_ERR_SHAPE),
+    (192, 128, dict(N=(1 << 31) // 192 - 100), qa.QM_ERR_SHAPE),   # one q/k head >= 2^31 elements
+    (192, 128, dict(dtype=3), qa.QM_ERR_DTYPE),
+    (192, 128, dict(scale=float("inf")), qa.QM_ERR_SCALE),
+    (192, 128, dict(causal=7), qa.QM_ERR_CAUSAL),
+    # B=1, H=2, N=128: q and k span 96 KiB at d_qk = 192, v 64 KiB at d_v = 128
+    (192, 128, dict(o=Q + 80 * 1024), qa.QM_ERR_ALIAS),          # inside q's wider extent
+    (192, 128, dict(lse=K + 90 * 1024), qa.QM_ERR_ALIAS),
+    (192, 128, dict(o=O + 8), qa.QM_ERR_UNSUPPORTED),
+], ids=lambda x: str(x))
+def test_mla_invalid_arguments_are_rejected(lib, d_qk, d_v, over, status):
+    assert call_mla(d_qk, d_v, **over) == status
+
+
+def test_plain_entry_rejects_the_mla_head(lib):
+    assert call(d=192) == qa.QM_ERR_HEADDIM
 
 
 def test_inputs_may_alias_each_other(lib):

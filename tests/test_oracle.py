@@ -150,6 +150,12 @@ def _kv_head_first(h, H, Hkv):
     return 0
 
 
+def _scores_truncated_to_value_width(Q, K, scale, causal, row0=0):
+    # scores over only the first 3/4 of the head (as if sized by the value width)
+    w = max(1, (Q.shape[1] * 3) // 4)
+    return _orig_scores(Q[:, :w], K[:, :w], scale, causal, row0)
+
+
 MUTANTS = {
     "scores_no_scale": ("scores_fp64", _scores_no_scale),
     "scores_fixed_scale": ("scores_fp64", _scores_fixed_scale),
@@ -170,6 +176,7 @@ MUTANTS = {
     "attention_drops_tail_rows": ("attention_fp64", _attention_last_row_block_dropped),
     "kv_head_interleaved": ("kv_head", _kv_head_modulo),
     "kv_head_always_first": ("kv_head", _kv_head_first),
+    "scores_truncated": ("scores_fp64", _scores_truncated_to_value_width),
 }
 
 
