@@ -37,7 +37,9 @@ blocking and no fusion.
 
 Readings where the paper is silent: the head layout is [B, H, N, d]; lse is
 the natural logarithm; the scale is applied to the exact dot product, never to
-16-bit Q.  Values may have their own head dimension d_v (the MLA shape the
+16-bit Q.  FP8 inputs (OCP E4M3 codes) come with per-tensor scale factors:
+the real tensors are the scaled decoded values, and the definition applies to
+those.  Values may have their own head dimension d_v (the MLA shape the
 paper evaluates: queries and keys 128 + 64 wide, values 128): the scores use
 all d columns of Q and K, the output has d_v columns.
 
@@ -49,14 +51,30 @@ from __future__ import annotations
 
 import numpy as np
 
-_F64_DTYPES = ("f16", "bf16", "f64")
+_F64_DTYPES = ("f16", "bf16", "e4m3", "f64")
+
+
+def _e4m3_value(c: int) -> float:
+    """OCP E4M3FN code c: sign, 4 exponent bits with bias 7, 3 mantissa bits;
+    exponent field 0 is subnormal (m/8 * 2^-6); S.1111.111 is NaN; no infinity."""
+    sign = -1.0 if c & 0x80 else 1.0
+    e, m = (c >> 3) & 0xF, c & 0x7
+    if e == 0xF and m == 0x7:
+        return float("nan")
+    if e == 0:
+        return sign * (m / 8.0) * 2.0 ** -6
+    return sign * (1.0 + m / 8.0) * 2.0 ** (e - 7)
+
+
+_E4M3_TABLE = np.array([_e4m3_value(c) for c in range(256)], dtype=np.float64)
 
 
 def decode_fp64(x: np.ndarray, dtype: str) -> np.ndarray:
     """Decode stored inputs to fp64, exactly.
 
     ``f16``: ``numpy.float16`` values; ``bf16``: ``uint16`` bit patterns (the
-    top half of an IEEE fp32); ``f64``: already fp64 (used by the pins).
+    top half of an IEEE fp32); ``e4m3``: ``uint8`` OCP E4M3FN codes (FP8);
+    ``f64``: already fp64 (used by the pins).
     """
     if dtype == "f16":
         if x.dtype != np.float16:
@@ -66,9 +84,19 @@ def decode_fp64(x: np.ndarray, dtype: str) -> np.ndarray:
         if x.dtype != np.uint16:
             raise TypeError("bf16 input must be uint16 bit patterns")
         return (x.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+    if dtype == "e4m3":
+        if x.dtype != np.uint8:
+            raise TypeError("e4m3 input must be uint8 codes")
+        return _E4M3_TABLE[x]
     if dtype == "f64":
         return np.asarray(x, dtype=np.float64)
     raise ValueError(f"unknown dtype {dtype!r}; expected one of {_F64_DTYPES}")
+
+
+def _descale(descale):
+    if descale is None:
+        return 1.0, 1.0, 1.0
+    return tuple(float(np.float32(t)) for t in descale)
 
 
 def kv_head(h: int, H: int, Hkv: int) -> int:
@@ -110,14 +138,18 @@ def softmax_rows_fp64(S: np.ndarray):
 
 
 def attention_fp64(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float,
-                   causal: bool, dtype: str, row_block: int = 256):
+                   causal: bool, dtype: str, row_block: int = 256, descale=None):
     """Exact attention forward for every (batch, head): q [B, H, N, d], k
     [B, Hkv, N, d] and v [B, Hkv, N, dv] with Hkv dividing H (Hkv = H:
     multi-head attention).
 
+    ``descale``: optional per-tensor factors (sq, sk, sv), taken as float32
+    values: the real tensors are sq*Q, sk*K and sv*V (FP8 inputs).
+
     Returns (O [B, H, N, dv] fp64, lse [B, H, N] fp64).
     """
     B, H, N, d = q.shape
+    sq, sk, sv = _descale(descale)
     Hkv = k.shape[1] if k.ndim == 4 else -1
     dv = v.shape[-1] if v.ndim == 4 else -1
     if k.shape != (B, Hkv, N, d) or v.shape != (B, Hkv, N, dv):
@@ -127,11 +159,11 @@ def attention_fp64(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float,
     lse = np.empty((B, H, N), dtype=np.float64)
     for b in range(B):
         for h in range(H):
-            K = decode_fp64(k[b, kv_head(h, H, Hkv)], dtype)
-            V = decode_fp64(v[b, kv_head(h, H, Hkv)], dtype)
+            K = decode_fp64(k[b, kv_head(h, H, Hkv)], dtype) * sk
+            V = decode_fp64(v[b, kv_head(h, H, Hkv)], dtype) * sv
             for r0 in range(0, N, row_block):
                 r1 = min(N, r0 + row_block)
-                Q = decode_fp64(q[b, h, r0:r1], dtype)
+                Q = decode_fp64(q[b, h, r0:r1], dtype) * sq
                 S = scores_fp64(Q, K, scale64, causal, row0=r0)
                 P, lse_blk = softmax_rows_fp64(S)
                 O[b, h, r0:r1] = P @ V
@@ -140,7 +172,7 @@ def attention_fp64(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float,
 
 
 def attention_rows_fp64(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float,
-                        causal: bool, dtype: str, rows):
+                        causal: bool, dtype: str, rows, descale=None):
     """Exact attention output for selected rows only.
 
     ``rows``: iterable of (b, h, i).  Returns (O [R, dv] fp64, lse [R] fp64) in
@@ -149,6 +181,7 @@ def attention_rows_fp64(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: floa
     query against all of its (visible) keys.
     """
     rows = [tuple(int(t) for t in r) for r in rows]
+    sq, sk, sv = _descale(descale)
     H = q.shape[1]
     Hkv = k.shape[1]
     O = np.empty((len(rows), v.shape[-1]), dtype=np.float64)
@@ -158,10 +191,10 @@ def attention_rows_fp64(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: floa
     for idx, (b, h, i) in enumerate(rows):
         by_head.setdefault((b, h), []).append((idx, i))
     for (b, h), items in by_head.items():
-        K = decode_fp64(k[b, kv_head(h, H, Hkv)], dtype)
-        V = decode_fp64(v[b, kv_head(h, H, Hkv)], dtype)
+        K = decode_fp64(k[b, kv_head(h, H, Hkv)], dtype) * sk
+        V = decode_fp64(v[b, kv_head(h, H, Hkv)], dtype) * sv
         for idx, i in items:
-            Q = decode_fp64(q[b, h, i:i + 1], dtype)
+            Q = decode_fp64(q[b, h, i:i + 1], dtype) * sq
             S = scores_fp64(Q, K, scale64, causal, row0=i)
             P, lse_row = softmax_rows_fp64(S)
             O[idx] = (P @ V)[0]

@@ -27,7 +27,7 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-DTYPES = ("f16", "bf16")
+DTYPES = ("f16", "bf16")   # 16-bit storage types of make_qkv; "e4m3" uses make_qkv_fp8
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -74,6 +74,48 @@ def make_qkv(B: int, H: int, N: int, d: int, dtype: str, seed: int = 0,
     return tuple(out)
 
 
+# ---------------------------------------------------------------- FP8 inputs
+# OCP E4M3FN: 1 sign, 4 exponent (bias 7) and 3 mantissa bits; no infinities;
+# S.1111.111 is NaN; the largest finite value is 448.  Non-negative finite
+# values in code order, for nearest-value rounding below.
+_E4M3_POS = np.array([(c & 7) / 8 * 2.0 ** -6 if (c >> 3) == 0 else
+                      (1 + (c & 7) / 8) * 2.0 ** ((c >> 3) - 7) for c in range(127)])
+E4M3_MAX = 448.0
+
+
+def f32_to_e4m3_bits(x: np.ndarray) -> np.ndarray:
+    """Round finite values with |x| <= 448 to OCP E4M3FN, to nearest with ties
+    to the even code (the even mantissa); return the uint8 codes."""
+    x = np.asarray(x, dtype=np.float64)
+    a = np.abs(x)
+    if not np.all(a <= E4M3_MAX):
+        raise ValueError("values beyond the E4M3 range (448) or NaN")
+    hi = np.clip(np.searchsorted(_E4M3_POS, a, side="left"), 0, 126)   # first value >= a
+    lo = np.clip(hi - 1, 0, 126)
+    dlo = a - _E4M3_POS[lo]
+    dhi = _E4M3_POS[hi] - a
+    take_hi = (dhi < dlo) | ((dhi == dlo) & (hi % 2 == 0))
+    code = np.where(take_hi, hi, lo).astype(np.uint8)
+    return np.where(np.signbit(x), code | 0x80, code).astype(np.uint8)   # keeps -0
+
+
+def make_qkv_fp8(B: int, H: int, N: int, d: int, seed: int = 0):
+    """FP8 inputs: Q, K, V drawn as ``make_qkv`` draws them (fp32 normals, Q then
+    K then V), each scaled per tensor so that its largest magnitude maps to 448,
+    rounded to E4M3.  Returns (q8, k8, v8, scales) with uint8 codes and the three
+    float32 descale factors: the real tensor is scale * decode(code)."""
+    rng = np.random.default_rng(seed)
+    out, scales = [], []
+    for _ in ("q", "k", "v"):
+        x = rng.standard_normal((B, H, N, d), dtype=np.float32)
+        s = np.float32(np.max(np.abs(x)) / np.float32(E4M3_MAX))
+        y = np.minimum(np.abs(x / s), np.float32(E4M3_MAX)) * np.sign(x)
+        out.append(f32_to_e4m3_bits(y))
+        scales.append(float(s))
+        del x, y
+    return out[0], out[1], out[2], tuple(scales)
+
+
 def default_scale(d: int) -> float:
     """The softmax scale 1/sqrt(d), as the fp32 value handed to the kernel."""
     return float(np.float32(1.0 / np.sqrt(np.float64(d))))
@@ -107,8 +149,14 @@ class Workload:
         return default_scale(self.d)   # 1/sqrt of the query/key head dimension
 
     def inputs(self):
+        if self.dtype == "e4m3":
+            raise ValueError("FP8 workloads draw their inputs with fp8_inputs()")
         return make_qkv(self.B, self.H, self.N, self.d, self.dtype,
                         seed=self.seed, qk_mult=self.qk_mult, Hkv=self.kv_heads, dv=self.d_v)
+
+    def fp8_inputs(self):
+        """(q8, k8, v8, (q_scale, k_scale, v_scale)) of an FP8 workload."""
+        return make_qkv_fp8(self.B, self.H, self.N, self.d, seed=self.seed)
 
 
 WORKLOADS = {
@@ -139,6 +187,10 @@ WORKLOADS = {
         Workload("mla_b1_h16_n4096_d192_dv128_bf16", 1, 16, 4096, 192, "bf16",
                  (False, True), dv=128),
         Workload("mla_b2_h4_n777_d192_dv128_f16", 2, 4, 777, 192, "f16", (False, True), dv=128),
+        # FP8 (OCP E4M3) inputs with per-tensor scales, bf16 output: the paper's
+        # FP8 table is MHA with the causal mask at d = 128
+        Workload("fp8_b2_h32_n8192_d128", 2, 32, 8192, 128, "e4m3", (False, True)),
+        Workload("fp8_b2_h3_n333_d128", 2, 3, 333, 128, "e4m3", (False, True)),
     )
 }
 

@@ -16,7 +16,9 @@ acceleration") fixes independently of any implementation:
   group's key/value head, equality with explicitly repeated key/value heads,
   identical query heads under multi-query attention;
 * values narrower than queries and keys (the MLA shape): the brute force, and
-  output columns that depend only on their own value column.
+  output columns that depend only on their own value column;
+* FP8 inputs: E4M3 decoding on known codes and against the library's own
+  float8 conversion, and the brute force on scaled FP8 inputs.
 
 ``tests/test_oracle.py`` runs every pin on the oracle and shows that planted
 mistakes in the oracle fail at least one pin.
@@ -43,6 +45,9 @@ def _decode_independent(x, dtype):
                for u in flat.view(np.uint16)]
     elif dtype == "bf16":
         out = [struct.unpack("<f", struct.pack("<I", int(u) << 16))[0] for u in flat]
+    elif dtype == "e4m3":
+        import torch   # the library's own FP8 decoding, independent of the oracle's table
+        return torch.from_numpy(np.ascontiguousarray(x)).view(torch.float8_e4m3fn).double().numpy()
     elif dtype == "f64":
         out = [float(t) for t in flat]
     else:
@@ -411,6 +416,42 @@ def pin_value_columns_independent(mod):
         _close(l2, lse, 0.0, "lse independent of V")
 
 
+def pin_e4m3_decode(mod):
+    """FP8 (OCP E4M3FN) decoding on known codes, and on all 256 codes against
+    the library's float8_e4m3fn conversion."""
+    codes = np.array([0x38, 0x7E, 0x01, 0x08, 0x80, 0xC5, 0x30, 0x07, 0x77], dtype=np.uint8)
+    expect = [1.0, 448.0, 2.0 ** -9, 2.0 ** -6, -0.0, -3.25, 0.5, 7 * 2.0 ** -9, 240.0]
+    got = list(mod.decode_fp64(codes, "e4m3"))
+    if got != expect or not math.copysign(1.0, got[4]) < 0:
+        raise AssertionError(f"e4m3 decode {got} != {expect}")
+    if not np.isnan(mod.decode_fp64(np.array([0x7F, 0xFF], dtype=np.uint8), "e4m3")).all():
+        raise AssertionError("S.1111.111 must decode to NaN")
+    allc = np.arange(256, dtype=np.uint8)
+    a = mod.decode_fp64(allc, "e4m3")
+    b = _decode_independent(allc, "e4m3")
+    same = (a == b) | (np.isnan(a) & np.isnan(b))
+    if not same.all():
+        raise AssertionError(f"e4m3 decode differs from the library at codes {np.nonzero(~same)[0][:5]}")
+
+
+def pin_fp8_brute_force(mod):
+    """FP8 inputs with per-tensor scales: the oracle equals the 50-digit brute
+    force on the scaled decoded values."""
+    from seeded_inputs import make_qkv_fp8
+    for N, d, scale, causal, seed in [(5, 8, 0.35, True, 61), (7, 16, 0.25, False, 62)]:
+        q, k, v, sc = make_qkv_fp8(1, 2, N, d, seed=seed)
+        O, lse = mod.attention_fp64(q, k, v, scale, causal, "e4m3", row_block=3, descale=sc)
+        s32 = float(np.float32(scale))
+        for h in range(2):
+            qf = _decode_independent(q[0, h], "e4m3") * float(np.float32(sc[0]))
+            kf = _decode_independent(k[0, h], "e4m3") * float(np.float32(sc[1]))
+            vf = _decode_independent(v[0, h], "e4m3") * float(np.float32(sc[2]))
+            Ob, lb = brute_force_decimal(qf, kf, vf, s32, causal)
+            tol = 1e-13 * (1.0 + abs(s32) * float(np.max(np.abs(qf @ kf.T))))
+            _close(O[0, h], Ob, tol * max(1.0, float(np.max(np.abs(vf)))), f"FP8 O N={N} d={d}")
+            _close(lse[0, h], lb, tol * max(1.0, float(np.max(np.abs(lb)))), f"FP8 lse N={N} d={d}")
+
+
 ALL_PINS = [
     pin_brute_force,
     pin_zero_query_mean,
@@ -430,4 +471,6 @@ ALL_PINS = [
     pin_mqa_identical_query_heads,
     pin_mla_brute_force,
     pin_value_columns_independent,
+    pin_e4m3_decode,
+    pin_fp8_brute_force,
 ]

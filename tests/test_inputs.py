@@ -1,5 +1,6 @@
 """The seeded input generator: determinism, rounding and recipe."""
 import numpy as np
+import pytest
 
 import seeded_inputs as si
 
@@ -51,3 +52,30 @@ def test_workloads():
     assert w.scale == float(np.float32(1 / np.sqrt(128)))
     long = si.WORKLOADS["mha_b1_h32_n32768_d128_bf16_causal_qk2"]
     assert long.qk_mult == 2.0 and long.causal == (True,)
+
+
+def test_e4m3_rounding_matches_the_library():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(5)
+    x = np.concatenate([rng.standard_normal(100000).astype(np.float32) * 60,
+                        rng.standard_normal(20000).astype(np.float32) * 1e-3,
+                        np.array([448, -448, 0, -0.0, 2 ** -10, 3 * 2 ** -10, 1.0625, 1.1875,
+                                  2 ** -6, -1.5 * 2 ** -9, 17, 464 - 1e-3], dtype=np.float32)])
+    x = np.clip(x, -448, 448)
+    mine = si.f32_to_e4m3_bits(x)
+    ref = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    assert np.array_equal(mine, ref)
+    with pytest.raises(ValueError):
+        si.f32_to_e4m3_bits(np.array([500.0]))
+
+
+def test_fp8_inputs_use_the_full_range():
+    q, k, v, sc = si.make_qkv_fp8(2, 3, 50, 16, seed=3)
+    for t, s in zip((q, k, v), sc):
+        assert t.dtype == np.uint8 and t.shape == (2, 3, 50, 16)
+        assert int((t & 0x7F).max()) == 0x7E          # the largest magnitude maps to 448
+        assert s > 0 and s == float(np.float32(s))
+    # the same fp32 draws as the 16-bit generator, scaled
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((2, 3, 50, 16), dtype=np.float32)
+    assert np.float32(np.max(np.abs(x)) / np.float32(448.0)) == np.float32(sc[0])

@@ -156,6 +156,19 @@ def _scores_truncated_to_value_width(Q, K, scale, causal, row0=0):
     return _orig_scores(Q[:, :w], K[:, :w], scale, causal, row0)
 
 
+def _decode_e4m3_bias8(x, dtype):
+    # the exponent bias of the other FP8 variant (E4M3 with bias 8)
+    if dtype == "e4m3":
+        return _orig_decode(x, dtype) / 2.0
+    return _orig_decode(x, dtype)
+
+
+def _attention_ignores_value_scale(q, k, v, scale, causal, dtype, row_block=256, descale=None):
+    if descale is not None:
+        descale = (descale[0], descale[1], 1.0)
+    return _orig_attention(q, k, v, scale, causal, dtype, row_block, descale)
+
+
 MUTANTS = {
     "scores_no_scale": ("scores_fp64", _scores_no_scale),
     "scores_fixed_scale": ("scores_fp64", _scores_fixed_scale),
@@ -177,6 +190,8 @@ MUTANTS = {
     "kv_head_interleaved": ("kv_head", _kv_head_modulo),
     "kv_head_always_first": ("kv_head", _kv_head_first),
     "scores_truncated": ("scores_fp64", _scores_truncated_to_value_width),
+    "decode_e4m3_bias8": ("decode_fp64", _decode_e4m3_bias8),
+    "attention_ignores_value_scale": ("attention_fp64", _attention_ignores_value_scale),
 }
 
 
