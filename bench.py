@@ -16,7 +16,7 @@ Prints one JSON line.  Extra objects:
                 the default workload): its algorithmic
                 flops per launch over its mean launch duration, timed with
                 HIP events on the launch stream inside the timed region,
-                against the dense bf16 MFMA peak; ``traffic`` is the HBM bytes
+                against the dense MFMA peak of the input type (bf16/fp16 2.5, FP8 5.0 PFLOP/s); ``traffic`` is the HBM bytes
                 per launch from rocprofv3 FETCH_SIZE + WRITE_SIZE counters
                 (scaled by a plain copy of known size), read from the
                 committed profile summary (default workload only), or null
@@ -44,6 +44,9 @@ import seeded_inputs as si  # noqa: E402
 METRIC = "attention fwd TFLOPS (4·B·H·N²·d, ½ if causal) and % of MFMA peak"
 PEAK_TFLOPS = 2500.0          # MI355X dense bf16/fp16 MFMA, published
 PEAK_FLOP_PER_CLK = 256 * 4096  # 256 CUs x 4096 dense bf16 flop per clock
+# FP8 (E4M3) MFMA: twice the 16-bit rate, 5.0 PFLOP/s dense, published
+PEAK_TFLOPS_FP8 = 5000.0
+PEAK_FLOP_PER_CLK_FP8 = 256 * 8192
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2506_12355_amd", "csrc", "attn_fwd_gfx950.hip")
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_fwd_bf16_d128_n8192_hbm_traffic.md")
 
@@ -134,22 +137,22 @@ class SclkSampler:
 def _oracle_head(args):
     from threadpoolctl import threadpool_limits
     from oracle import attention_fp64
-    q, k, v, scale, dtype, masks = args
+    q, k, v, scale, dtype, masks, descale = args
     with threadpool_limits(limits=1):
         t0 = time.perf_counter()
         for causal in masks:
-            attention_fp64(q, k, v, scale, causal, dtype)
+            attention_fp64(q, k, v, scale, causal, dtype, descale=descale)
         return time.perf_counter() - t0
 
 
-def cpu_baseline(w, q, k, v, max_workers=16):
+def cpu_baseline(w, q, k, v, max_workers=16, descale=None):
     import multiprocessing as mp
     cores = max(1, min(max_workers, len(os.sched_getaffinity(0))))
     n_heads = min(w.B * w.H, 4 * cores)
     group = w.H // w.kv_heads
     heads = [(i // w.H, i % w.H) for i in range(n_heads)]
     jobs = [(q[b:b + 1, h:h + 1].copy(), k[b:b + 1, h // group:h // group + 1].copy(),
-             v[b:b + 1, h // group:h // group + 1].copy(), w.scale, w.dtype, w.causal)
+             v[b:b + 1, h // group:h // group + 1].copy(), w.scale, w.dtype, w.causal, descale)
             for b, h in heads]
     ctx = mp.get_context("fork")
     t0 = time.perf_counter()
@@ -248,15 +251,21 @@ def main():
         return
 
     w = si.WORKLOADS[args.workload]
-    q, k, v = w.inputs()
+    fp8 = w.dtype == "e4m3"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    tdtype = torch.bfloat16 if w.dtype == "bf16" else torch.float16
-
-    def dev16(x):
-        return torch.from_numpy(x.view(np.int16)).to(dev).view(tdtype)
-
-    tq, tk, tv = dev16(q), dev16(k), dev16(v)
+    if fp8:
+        # E4M3 codes with per-tensor scales; the output is bf16
+        q, k, v, scales = w.fp8_inputs()
+        tdtype = torch.bfloat16
+        tq, tk, tv = (torch.from_numpy(x).to(dev).view(torch.float8_e4m3fn) for x in (q, k, v))
+    else:
+        q, k, v = w.inputs()
+        scales = None
+        tdtype = torch.bfloat16 if w.dtype == "bf16" else torch.float16
+        tq, tk, tv = (torch.from_numpy(x.view(np.int16)).to(dev).view(tdtype) for x in (q, k, v))
+    peak = PEAK_TFLOPS_FP8 if fp8 else PEAK_TFLOPS
+    peak_per_clk = PEAK_FLOP_PER_CLK_FP8 if fp8 else PEAK_FLOP_PER_CLK
     masks = list(w.causal)
     outs = [(torch.empty((w.B, w.H, w.N, w.d_v), dtype=tdtype, device=dev),
              torch.empty((w.B, w.H, w.N), dtype=torch.float32, device=dev))
@@ -267,8 +276,12 @@ def main():
         for m, causal in enumerate(masks):
             if ev is not None:
                 ev[m].record(stream)
-            qa.fwd(tq, tk, tv, causal=causal, scale=w.scale, out=outs[m][0], lse=outs[m][1],
-                   stream=stream)
+            if fp8:
+                qa.fwd_fp8(tq, tk, tv, scales, causal=causal, scale=w.scale, out=outs[m][0],
+                           lse=outs[m][1], stream=stream)
+            else:
+                qa.fwd(tq, tk, tv, causal=causal, scale=w.scale, out=outs[m][0],
+                       lse=outs[m][1], stream=stream)
         if ev is not None:
             ev[len(masks)].record(stream)
 
@@ -321,9 +334,9 @@ def main():
             "flop_count": ("4·B·H·N²·d" if w.d_v == w.d else "2·B·H·N²·(d + d_v)") + ", ½ if causal",
             "masks": ["causal" if c else "none" for c in masks], "seed": w.seed,
         },
-        "pct_of_peak": round(100.0 * value / PEAK_TFLOPS, 2),
+        "pct_of_peak": round(100.0 * value / peak, 2),
         "sclk_mhz": sclk.median(),
-        "pct_of_peak_at_sclk": (round(100.0 * value / (PEAK_FLOP_PER_CLK * sclk.median() * 1e6 / 1e12), 2)
+        "pct_of_peak_at_sclk": (round(100.0 * value / (peak_per_clk * sclk.median() * 1e6 / 1e12), 2)
                                 if sclk.median() else None),
         "per_launch": {
             name: {"ms": round(ms, 4), "tflops": round(f / (ms * 1e-3) / 1e12, 2)}
@@ -333,14 +346,14 @@ def main():
             "bound": "mfma",
             "kernel": f"attn_fwd_kernel<{w.d}, {w.d_v}, {w.dtype}, {mask_name[0]}>",
             "achieved": round(achieved, 2),
-            "peak": PEAK_TFLOPS,
+            "peak": peak,
             "unit": "TFLOP/s",
-            "frac": round(achieved / PEAK_TFLOPS, 4),
+            "frac": round(achieved / peak, 4),
             "traffic": committed_traffic() if w.name == si.BENCH_WORKLOAD else None,
         },
     }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(w, q, k, v)
+        result["cpu_baseline"] = cpu_baseline(w, q, k, v, descale=scales)
     print(json.dumps(result), flush=True)
 
 

@@ -43,7 +43,7 @@ typedef enum {
   QM_BF16 = 1  /* bfloat16 (top half of an IEEE binary32) */
 } qm_dtype_t;
 
-/* Status codes returned by qm_attn_fwd, qm_attn_fwd_gqa and qm_attn_fwd_mla. */
+/* Status codes returned by every qm_attn_fwd* entry point. */
 enum {
   QM_OK = 0,
   QM_ERR_NULL = -1,        /* q, k, v, o or lse is NULL */
@@ -52,7 +52,8 @@ enum {
   QM_ERR_HEADDIM = -3,     /* d is not 64 or 128 (qm_attn_fwd_mla: (d_qk, d_v) is not
                               (64, 64), (128, 128) or (192, 128)) */
   QM_ERR_DTYPE = -4,       /* dtype is not QM_F16 or QM_BF16 */
-  QM_ERR_SCALE = -5,       /* scale is infinite or NaN */
+  QM_ERR_SCALE = -5,       /* scale (or an FP8 tensor scale) is infinite or NaN, or the
+                              combined scale times log2(e) overflows fp32 */
   QM_ERR_ALIAS = -6,       /* o or lse overlaps q, k, v or each other */
   QM_ERR_CAUSAL = -7,      /* causal is neither 0 nor 1 */
   QM_ERR_LAUNCH = -8,      /* the HIP runtime rejected the kernel launch */
@@ -132,6 +133,31 @@ int qm_attn_fwd_gqa(const void* q, const void* k, const void* v, void* o, float*
 int qm_attn_fwd_mla(const void* q, const void* k, const void* v, void* o, float* lse,
                     int B, int H, int N, int d_qk, int d_v, float scale, int causal,
                     hipStream_t stream, int dtype);
+
+/*
+ * qm_attn_fwd_fp8 - attention forward on FP8 inputs, the variant the paper's
+ * case study generates (its FP8 table: MHA with the causal mask at head
+ * dimension 128).  q, k and v hold OCP E4M3 codes (1 sign, 4 exponent bits
+ * with bias 7, 3 mantissa bits; the largest value 448), each with one scale
+ * factor for the whole tensor: the operation is qm_attn_fwd's on the real
+ * tensors q_scale*Q, k_scale*K and v_scale*V.  The products run on the FP8
+ * matrix cores with fp32 accumulation; the probabilities are rounded to E4M3
+ * (to nearest even) before the second product; per output row i that bounds
+ * the error by 2^-4 sum_j P_ij |v_j| + 2^-10 exp(m_i - lse_i) sum_j |v_j| (P the
+ * exact probabilities, m_i the row's largest score, v the real values), and the
+ * row sums and lse stay in fp32.
+ *
+ *   q, k, v  [in]  device, [B][H][N][d] uint8 E4M3 codes.
+ *   o        [out] device, [B][H][N][d] bfloat16 (round to nearest even).
+ *   lse      [out] device, [B][H][N] float32, of the scaled scores.
+ *   d              128; any other value: QM_ERR_HEADDIM.
+ *   q_scale, k_scale, v_scale   finite per-tensor factors (QM_ERR_SCALE otherwise).
+ *   scale          finite, multiplies the dot product of the real tensors.
+ *   B, H, N, causal, stream: as for qm_attn_fwd; there is no dtype argument.
+ */
+int qm_attn_fwd_fp8(const void* q, const void* k, const void* v, void* o, float* lse,
+                    int B, int H, int N, int d, float q_scale, float k_scale, float v_scale,
+                    float scale, int causal, hipStream_t stream);
 
 /* qm_attn_strerror - a static, human-readable string for a status code. */
 const char* qm_attn_strerror(int status);

@@ -3,7 +3,8 @@
 ``fwd(q, k, v, causal, scale)`` computes softmax(mask(scale * Q K^T)) V and the
 per-row log-sum-exp for [B, H, N, d] fp16/bf16 tensors on one GPU; k and v may
 have fewer heads than q (grouped-query and multi-query attention), and v a
-narrower head than q and k (the MLA shape, 192/128).  The
+narrower head than q and k (the MLA shape, 192/128).  ``fwd_fp8`` takes FP8
+(E4M3) inputs with per-tensor scales.  The
 operation and its arguments are documented in ``include/qm_attn.h``.
 """
 from .binding import (  # noqa: F401
@@ -22,8 +23,10 @@ from .binding import (  # noqa: F401
     QM_OK,
     QmAttnError,
     fwd,
+    fwd_fp8,
     load_library,
     qm_attn_fwd,
+    qm_attn_fwd_fp8,
     qm_attn_fwd_gqa,
     qm_attn_fwd_mla,
     strerror,

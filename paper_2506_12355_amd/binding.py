@@ -70,6 +70,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
             ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
         ]
         lib.qm_attn_fwd_mla.restype = ctypes.c_int
+        lib.qm_attn_fwd_fp8.argtypes = [
+            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+            ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+            ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_int,
+            ctypes.c_void_p,
+        ]
+        lib.qm_attn_fwd_fp8.restype = ctypes.c_int
         lib.qm_attn_strerror.argtypes = [ctypes.c_int]
         lib.qm_attn_strerror.restype = ctypes.c_char_p
         _lib = lib
@@ -96,6 +103,53 @@ def qm_attn_fwd_mla(q, k, v, o, lse, B, H, N, d_qk, d_v, scale, causal, stream, 
     """The unequal-head-dimension C entry point with plain integers for pointers."""
     return load_library().qm_attn_fwd_mla(q, k, v, o, lse, int(B), int(H), int(N), int(d_qk),
                                           int(d_v), float(scale), int(causal), stream, int(dtype))
+
+
+def qm_attn_fwd_fp8(q, k, v, o, lse, B, H, N, d, q_scale, k_scale, v_scale, scale, causal,
+                    stream) -> int:
+    """The FP8 C entry point with plain integers for pointers; returns the status."""
+    return load_library().qm_attn_fwd_fp8(q, k, v, o, lse, int(B), int(H), int(N), int(d),
+                                          float(q_scale), float(k_scale), float(v_scale),
+                                          float(scale), int(causal), stream)
+
+
+def fwd_fp8(q, k, v, scales, causal: bool = False, scale: float | None = None, out=None,
+            lse=None, stream=None):
+    """FP8 attention forward: q, k, v are [B, H, N, d] tensors of OCP E4M3 codes
+    (``torch.float8_e4m3fn`` or ``uint8``) on a ROCm device, ``scales`` the three
+    per-tensor factors (q_scale, k_scale, v_scale).  Returns (o, lse): o bf16
+    [B, H, N, d], lse float32 [B, H, N].  ``scale`` defaults to 1/sqrt(d)
+    rounded to float32."""
+    import torch
+
+    for t in (q, k, v):
+        if t.dim() != 4 or t.shape != q.shape:
+            raise ValueError("q, k and v must share the shape [B, H, N, d]")
+        if t.dtype not in (torch.uint8, torch.float8_e4m3fn):
+            raise TypeError("FP8 inputs must be float8_e4m3fn or uint8 codes")
+        if not t.is_cuda or t.device != q.device or not t.is_contiguous():
+            raise ValueError("q, k and v must be contiguous tensors on one ROCm device")
+    B, H, N, d = q.shape
+    if scale is None:
+        scale = float(torch.tensor(1.0 / d ** 0.5, dtype=torch.float32))
+    if out is None:
+        out = torch.empty((B, H, N, d), dtype=torch.bfloat16, device=q.device)
+    elif out.shape != q.shape or out.dtype != torch.bfloat16 or not out.is_contiguous():
+        raise ValueError("out must be a contiguous bfloat16 tensor like q")
+    if lse is None:
+        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    elif lse.shape != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous():
+        raise ValueError("lse must be a contiguous float32 tensor of shape [B, H, N]")
+    if stream is None:
+        stream = torch.cuda.current_stream(q.device)
+    qs, ks, vs = (float(t) for t in scales)
+    with torch.cuda.device(q.device):
+        status = qm_attn_fwd_fp8(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                 lse.data_ptr(), B, H, N, d, qs, ks, vs, scale,
+                                 1 if causal else 0, stream.cuda_stream)
+    if status != QM_OK:
+        raise QmAttnError(status, strerror(status))
+    return out, lse
 
 
 def _dtype_code(t) -> int:

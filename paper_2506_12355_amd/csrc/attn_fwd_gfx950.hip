@@ -76,9 +76,12 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef int32_t i32x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+typedef int32_t i32x8 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) i32x2 lds_i32x2;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 
@@ -96,9 +99,9 @@ constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data
 constexpr int kWaitLoads = 0x0070;
 
 struct KParams {
-  const uint16_t* q;
-  const uint16_t* k;
-  const uint16_t* v;
+  const uint8_t* q;   // 16-bit or FP8 elements, addressed in bytes
+  const uint8_t* k;
+  const uint8_t* v;
   uint16_t* o;
   float* lse;
   int N;
@@ -108,7 +111,8 @@ struct KParams {
   int nq;           // query blocks per head
   int wg_per_head;  // workgroups per head: nq, or ceil(nq / 2) pairs when causal
   int total;        // wg_per_head * B * H workgroups
-  float c;     // |scale| * log2 e
+  float c;     // |scale| * log2 e (FP8: |scale * q_scale * k_scale| * log2 e)
+  float vscale;  // factor of O: 1, or the FP8 value scale
   int qmode;
 };
 
@@ -139,21 +143,51 @@ struct Half<1> {  // bf16
   }
 };
 
-// LDS layout of one K or V tile (kBN rows of D 16-bit values).  One direct
-// load writes 1 KB = RPL whole rows; load group g holds rows g, g + NG,
-// g + 2 NG, ... (NG groups), and groups are padded: K by 16 bytes, V by 64
-// bytes.  Then a 128-bit K read of 16 consecutive rows in one column, and a
-// transposing V read of 4 consecutive rows x 4 consecutive 16-byte units,
-// each touch 16 distinct bank groups, and every operand address is a per-lane
-// base plus a compile-time offset.
-template <int D>
+// FP8 (OCP E4M3) operands: the 32x32x64 MFMA, 32 one-byte values per lane
+// (lane l: row or column l % 32, k = 32 (l / 32) + byte), unit block scales,
+// and the fp32 -> E4M3 pack of two values into one half of a word (round to
+// nearest even; the values packed here are at most 2^8, below the 448 limit).
+struct Fp8 {
+  static __device__ __forceinline__ f32x16 mfma(i32x8 a, i32x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
+  }
+  template <bool HIGH>   // into bits 16..31 (else 0..15) of old
+  static __device__ __forceinline__ int32_t pack(float x, float y, int32_t old) {
+    return __builtin_amdgcn_cvt_pk_fp8_f32(x, y, old, HIGH);
+  }
+};
+
+// Operand traits: DT 0 = fp16, 1 = bf16 (16-bit operands, 32x32x16 MFMA),
+// 2 = FP8 E4M3 (32x32x64 MFMA, bf16 output).
+template <int DT>
+struct Ops {
+  static constexpr bool kFp8 = DT == 2;
+  static constexpr int ES = kFp8 ? 1 : 2;        // bytes per input element
+  static constexpr int KSTEP = kFp8 ? 64 : 16;   // MFMA contraction length
+  static constexpr int KGB = KSTEP / 2 * ES;     // bytes of one lane's k-group
+  using Frag = typename std::conditional<kFp8, i32x8, u32x4>::type;
+  static __device__ __forceinline__ f32x16 mfma(Frag a, Frag b, f32x16 c) {
+    if constexpr (kFp8) return Fp8::mfma(a, b, c);
+    else return Half<DT>::mfma(a, b, c);
+  }
+};
+
+// LDS layout of one K or V tile (kBN rows of ROWB bytes).  One direct load
+// writes 1 KB = RPL whole rows; load group g holds rows g, g + NG, g + 2 NG,
+// ... (NG groups), and groups are padded: K by 16 bytes, V by VPAD bytes (64
+// for the 16-bit transposing reads, 16 for the byte ones).  Then a 128-bit K
+// read of 16 consecutive rows in one column, and a transposing V read (16-bit:
+// 4 consecutive rows x 4 consecutive 16-byte units; bytes: 4 rows of two
+// groups x two 8-byte units), each touch distinct banks, and every operand
+// address is a per-lane base plus a compile-time offset.
+template <int ROWB, int VPAD = 64>
 struct Layout {
-  static constexpr int U = D / 8;                 // 16-byte units per row
+  static constexpr int U = ROWB / 16;             // 16-byte units per row
   static constexpr int ROW = 16 * U;              // bytes per row
   static constexpr int RPL = 64 / U;              // rows per 1 KB load
   static constexpr int NG = kBN / RPL;            // load groups per tile
   static constexpr int KGS = 1024 + 16;           // K group stride (bytes)
-  static constexpr int VGS = 1024 + 64;           // V group stride (bytes)
+  static constexpr int VGS = 1024 + VPAD;         // V group stride (bytes)
   static constexpr int KBYTES = NG * KGS;
   static constexpr int VBYTES = NG * VGS;
   static constexpr int BUF = KBYTES + VBYTES;     // one K tile + one V tile
@@ -162,16 +196,17 @@ struct Layout {
   static_assert(BUF % 16 == 0, "buffers stay 16-byte aligned");
 };
 
-// LDS layout of one K tile of DK columns: the first min(DK, 128) columns as a
-// Layout part, and (DK = 192) the remaining 64 columns as a second part right
-// after it.  Each part keeps whole rows per direct load.
-template <int DK>
+// LDS layout of one K tile of DK columns of ES-byte elements: the first
+// min(DK, 128) columns as a Layout part, and (DK = 192) the remaining 64
+// columns as a second part right after it.  Each part keeps whole rows per
+// direct load.
+template <int DK, int ES = 2, int KSTEP = 16>
 struct KTile {
   static constexpr int W0 = DK < 128 ? DK : 128;  // columns of part 0
   static constexpr int W1 = DK - W0;              // columns of part 1 (0 or 64)
-  using L0 = Layout<W0>;
-  using L1 = Layout<W1 ? W1 : 64>;                // unused when W1 == 0
-  static constexpr int NKS0 = W0 / 16;            // GEMM-I k-steps in part 0
+  using L0 = Layout<W0 * ES>;
+  using L1 = Layout<W1 ? W1 * ES : 128>;          // unused when W1 == 0
+  static constexpr int NKS0 = W0 / KSTEP;         // GEMM-I k-steps in part 0
   static constexpr int OFF1 = L0::NG * L0::KGS;   // byte offset of part 1
   static constexpr int BYTES = OFF1 + (W1 ? L1::NG * L1::KGS : 0);
   static constexpr int GPW0 = L0::NG / kWaves;    // direct loads per wave, part 0
@@ -183,14 +218,20 @@ struct KTile {
 // Depth of the K and V rings: four 64-key blocks (one barrier per two blocks)
 // when four K and four V tiles fit the 160 KB of LDS, else two (one barrier
 // per block).
-template <int DK, int DV>
+template <int DK, int DV, int DT>
+using KTileOf = KTile<DK, Ops<DT>::ES, Ops<DT>::KSTEP>;
+template <int DV, int DT>
+using VTileOf = Layout<DV * Ops<DT>::ES, Ops<DT>::kFp8 ? 16 : 64>;
+
+template <int DK, int DV, int DT>
 constexpr int ring_depth() {
-  return 4 * (KTile<DK>::BYTES + Layout<DV>::VBYTES) <= 160 * 1024 ? 4 : 2;
+  return 4 * (KTileOf<DK, DV, DT>::BYTES + VTileOf<DV, DT>::VBYTES) <= 160 * 1024 ? 4 : 2;
 }
 
-template <int DK, int DV>
+template <int DK, int DV, int DT>
 constexpr size_t lds_bytes() {
-  return (size_t)ring_depth<DK, DV>() * (KTile<DK>::BYTES + Layout<DV>::VBYTES);
+  return (size_t)ring_depth<DK, DV, DT>() *
+         (KTileOf<DK, DV, DT>::BYTES + VTileOf<DV, DT>::VBYTES);
 }
 
 // Slot of exponential chunk c (of 16) in region 1 of NSLOT slots, and the
@@ -257,12 +298,16 @@ __device__ __forceinline__ void lds_load16(i32x4 rs, uint32_t lds, uint32_t voff
 
 template <int DK, int DV, int DT, bool CAUSAL>
 __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
-  using KT = KTile<DK>;                  // K tile (DK columns)
-  using LV = Layout<DV>;                 // V tile (DV columns)
-  constexpr int NKS = DK / 16;           // GEMM-I k-steps
+  using OP = Ops<DT>;
+  using Frag = typename OP::Frag;        // one MFMA A or B operand
+  constexpr bool FP8 = OP::kFp8;
+  constexpr int ES = OP::ES;             // bytes per input element
+  using KT = KTileOf<DK, DV, DT>;        // K tile (DK columns)
+  using LV = VTileOf<DV, DT>;            // V tile (DV columns)
+  constexpr int NKS = DK / OP::KSTEP;    // GEMM-I k-steps
   constexpr int NMT = DV / 32;           // GEMM-II M tiles
   constexpr int GPWV = LV::NG / kWaves;  // V direct loads per wave per block
-  constexpr int RING = ring_depth<DK, DV>();
+  constexpr int RING = ring_depth<DK, DV, DT>();
 
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   char* const lds = reinterpret_cast<char*>(smem);
@@ -294,11 +339,11 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
   // workgroups run on one XCD and share its L2 for the K/V stream.
   const int b = bh / p.H;
   const int bhkv = b * p.Hkv + (bh - b * p.H) / p.group;
-  const uint32_t head_bytes_k = (uint32_t)N * DK * 2;   // one head of q or k
-  const uint32_t head_bytes_v = (uint32_t)N * DV * 2;   // one head of v or o
-  const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + (size_t)bh * N * DK, head_bytes_k);
-  const i32x4 rk = make_dma_rsrc(p.k + (size_t)bhkv * N * DK, head_bytes_k);
-  const i32x4 rv = make_dma_rsrc(p.v + (size_t)bhkv * N * DV, head_bytes_v);
+  const uint32_t head_bytes_k = (uint32_t)N * DK * ES;  // one head of q or k
+  const uint32_t head_bytes_v = (uint32_t)N * DV * ES;  // one head of v
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + (size_t)bh * N * DK * ES, head_bytes_k);
+  const i32x4 rk = make_dma_rsrc(p.k + (size_t)bhkv * N * DK * ES, head_bytes_k);
+  const i32x4 rv = make_dma_rsrc(p.v + (size_t)bhkv * N * DV * ES, head_bytes_v);
   // zero-size descriptors: a load through one touches no memory and writes zeros
   const i32x4 rk0 = i32x4{rk[0], rk[1], 0, rk[3]};
   const i32x4 rv0 = i32x4{rv[0], rv[1], 0, rv[3]};
@@ -309,12 +354,22 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     const int qrow = qw + l32;       // the query row whose column this lane holds
 
     // ---- Q: B operand of GEMM-I, resident for the whole key loop ----
-    u32x4 qf[NKS];
+    // lane: query row qrow, k-group hi (OP::KGB bytes of each k-step)
+    Frag qf[NKS];
   #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
-      qf[ks] = __builtin_amdgcn_raw_buffer_load_b128(rq, (uint32_t)(qrow * DK + 16 * ks + 8 * hi) * 2, 0, 0);
-      if (p.qmode == kQNegate) qf[ks] ^= 0x80008000u;
-      if (p.qmode == kQZero) qf[ks] = u32x4{0, 0, 0, 0};
+      const uint32_t off = (uint32_t)(qrow * DK * ES + ks * OP::KSTEP * ES + hi * OP::KGB);
+      if constexpr (FP8) {
+        const u32x4 lo = __builtin_amdgcn_raw_buffer_load_b128(rq, off, 0, 0);
+        const u32x4 up = __builtin_amdgcn_raw_buffer_load_b128(rq, off + 16, 0, 0);
+        qf[ks] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
+                       (int)up[0], (int)up[1], (int)up[2], (int)up[3]};
+        if (p.qmode == kQNegate) qf[ks] ^= (int)0x80808080u;
+      } else {
+        qf[ks] = __builtin_amdgcn_raw_buffer_load_b128(rq, off, 0, 0);
+        if (p.qmode == kQNegate) qf[ks] ^= 0x80008000u;
+      }
+      if (p.qmode == kQZero) qf[ks] = Frag{};
     }
 
     const int kv_end = CAUSAL ? min(N, q0 + kBM) : N;
@@ -331,28 +386,28 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     constexpr int VOFF = RING * KT::BYTES;
     // lane parts of the global offsets (row slot, 16-byte unit, column of the
     // K part); the row of the load group is added per load
-    const uint32_t koff0 = (uint32_t)(KT::L0::NG * (lane / KT::L0::U) * DK * 2 + (lane % KT::L0::U) * 16);
-    const uint32_t koff1 = (uint32_t)(KT::L1::NG * (lane / KT::L1::U) * DK * 2 + KT::W0 * 2 +
+    const uint32_t koff0 = (uint32_t)(KT::L0::NG * (lane / KT::L0::U) * DK * ES + (lane % KT::L0::U) * 16);
+    const uint32_t koff1 = (uint32_t)(KT::L1::NG * (lane / KT::L1::U) * DK * ES + KT::W0 * ES +
                                       (lane % KT::L1::U) * 16);
-    const uint32_t voff = (uint32_t)(LV::NG * (lane / LV::U) * DV * 2 + (lane % LV::U) * 16);
+    const uint32_t voff = (uint32_t)(LV::NG * (lane / LV::U) * DV * ES + (lane % LV::U) * 16);
     auto lds_addr = [&](int byte_off) { return (uint32_t)(uintptr_t)(lds_void*)(lds + byte_off); };
     // load i (of KT::GPW) of this wave for K block blk into K slot kb
     auto k_load = [&](int i, int blk, int kb, i32x4 rs) __attribute__((always_inline)) {
       if (i < KT::GPW0) {
         const int g = wave * KT::GPW0 + i;
         lds_load16(rs, lds_addr(kb * KT::BYTES + g * KT::L0::KGS),
-                   koff0 + (uint32_t)((blk * kBN + g) * DK) * 2);
+                   koff0 + (uint32_t)((blk * kBN + g) * DK) * ES);
       } else {
         const int g = wave * KT::GPW1 + (i - KT::GPW0);
         lds_load16(rs, lds_addr(kb * KT::BYTES + KT::OFF1 + g * KT::L1::KGS),
-                   koff1 + (uint32_t)((blk * kBN + g) * DK) * 2);
+                   koff1 + (uint32_t)((blk * kBN + g) * DK) * ES);
       }
     };
     // load i (of GPWV) of this wave for V block blk into V slot vb
     auto v_load = [&](int i, int blk, int vb, i32x4 rs) __attribute__((always_inline)) {
       const int g = wave * GPWV + i;
       lds_load16(rs, lds_addr(VOFF + vb * LV::VBYTES + g * LV::VGS),
-                 voff + (uint32_t)((blk * kBN + g) * DV) * 2);
+                 voff + (uint32_t)((blk * kBN + g) * DV) * ES);
     };
     auto load_k = [&](int blk, int kb) {
   #pragma unroll
@@ -394,23 +449,38 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     // per-lane LDS byte bases of the operand reads; every read adds a constant
     //   K (A of GEMM-I): row r = 32 kt + l32 -> group r % NG, slot r / NG of
     //   its part; unit 2 ks + hi
-    const int k_base0 = (l32 % KT::L0::NG) * KT::L0::KGS + (l32 / KT::L0::NG) * KT::L0::ROW + 16 * hi;
+    const int k_base0 = (l32 % KT::L0::NG) * KT::L0::KGS + (l32 / KT::L0::NG) * KT::L0::ROW +
+                        OP::KGB * hi;
     const int k_base1 = KT::OFF1 + (l32 % KT::L1::NG) * KT::L1::KGS +
-                        (l32 / KT::L1::NG) * KT::L1::ROW + 16 * hi;
+                        (l32 / KT::L1::NG) * KT::L1::ROW + OP::KGB * hi;
     //   V (A of GEMM-II, transposing read): key = 16 u + 8 h2 + kq, dims d0 .. d0+3
     const int grp = lane >> 4;
     const int sl = lane & 15;
     const int kq = 4 * (grp >> 1) + (sl >> 2);
     const int v_base = VOFF + kq * LV::VGS + 2 * (16 * (grp & 1) + 4 * (sl & 3));
+    //   V, FP8 (byte-transposing read; within each 16-lane group G, output lane
+    //   i, byte r is byte i % 8 of source lane 2 r + i / 8): source lane
+    //   2 r + e of group G reads 8 bytes of key 32 (t/2) + 16 (t%2) + 8 (r/4) +
+    //   4 (G/2) + r%4 (read t of 4), columns 32 mt + 16 (G%2) + 8 e onward, so
+    //   that output lane l gets column 32 mt + l%32 of exactly the keys its P
+    //   bytes hold (byte j: key 32 (j/16) + 8 ((j/4)%4) + 4 (l/32) + j%4)
+    const int v8_base = VOFF + (4 * (grp >> 1) + ((sl >> 1) & 3)) * LV::VGS +
+                        (sl >> 3) * LV::ROW + 16 * (grp & 1) + 8 * (sl & 1);
 
     auto k_read = [&](int kb, int kt, int ks) {
-      if (ks < KT::NKS0) {
-        return *reinterpret_cast<const u32x4*>(lds + kb * KT::BYTES + k_base0 +
-                                               kt * (32 / KT::L0::NG) * KT::L0::ROW + 32 * ks);
+      constexpr int KSB = OP::KSTEP * ES;   // bytes per k-step of a row
+      const char* a = (ks < KT::NKS0)
+          ? lds + kb * KT::BYTES + k_base0 + kt * (32 / KT::L0::NG) * KT::L0::ROW + KSB * ks
+          : lds + kb * KT::BYTES + k_base1 + kt * (32 / KT::L1::NG) * KT::L1::ROW +
+                KSB * (ks - KT::NKS0);
+      if constexpr (FP8) {
+        const u32x4 lo = *reinterpret_cast<const u32x4*>(a);
+        const u32x4 up = *reinterpret_cast<const u32x4*>(a + 16);
+        return i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
+                     (int)up[0], (int)up[1], (int)up[2], (int)up[3]};
+      } else {
+        return *reinterpret_cast<const u32x4*>(a);
       }
-      return *reinterpret_cast<const u32x4*>(lds + kb * KT::BYTES + k_base1 +
-                                             kt * (32 / KT::L1::NG) * KT::L1::ROW +
-                                             32 * (ks - KT::NKS0));
     };
     auto v_read = [&](int vb, int mt, int u, int h2) {
       // group of key 16 u + 8 h2 + kq is (16 u + 8 h2) % NG + kq, slot (16 u + 8 h2) / NG
@@ -430,7 +500,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
   #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) {
   #pragma unroll
-        for (int kt = 0; kt < 2; ++kt) s[kt] = Half<DT>::mfma(k_read(kb, kt, ks), qf[ks], s[kt]);
+        for (int kt = 0; kt < 2; ++kt) s[kt] = OP::mfma(k_read(kb, kt, ks), qf[ks], s[kt]);
       }
     };
 
@@ -458,15 +528,15 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     auto block = [&](auto ph, int j, int kb_next, int vb, f32x16 (&s)[2], f32x16 (&s_next)[2])
         __attribute__((always_inline)) {
       const int j0 = j * kBN;
-      constexpr int AHEAD = 4;
+      constexpr int AHEAD = FP8 ? 2 : 4;              // operand reads ahead of their MFMA
       constexpr int NG1 = 2 * NKS;                    // GEMM-I MFMAs per block
       constexpr int NSLOT = NG1 > 16 ? NG1 : 16;      // slots of region 1
-      constexpr int NV = 4 * NMT;                     // GEMM-II MFMAs per block
+      constexpr int NV = FP8 ? NMT : 4 * NMT;         // GEMM-II MFMAs per block
       constexpr int NDMA = n_dma(decltype(ph){});     // direct loads in this block
       constexpr int DSTRIDE = (NSLOT / 2) / NDMA > 0 ? (NSLOT / 2) / NDMA : 1;
       // first K fragments of GEMM-I for block j+1: their LDS latency runs under
       // the mask work below
-      u32x4 kring[AHEAD];
+      Frag kring[AHEAD];
   #pragma unroll
       for (int m = 0; m < AHEAD; ++m) kring[m] = k_read(kb_next, m % 2, m / 2);
 
@@ -489,13 +559,44 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
       // GEMM-II operand: V^T fragment t (M tile t % NMT, key step t / NMT), so
       // consecutive MFMAs accumulate into different O tiles
       auto v_frag = [&](int t) __attribute__((always_inline)) {
-        const int mt = t % NMT, u = t / NMT;
-        const u32x2 a0 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 0));
-        const u32x2 a1 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 1));
-        return u32x4{a0[0], a0[1], a1[0], a1[1]};
+        if constexpr (FP8) {
+          // M tile t, all 64 keys: four byte-transposing reads of 8 bytes
+          i32x8 f;
+  #pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const i32x2 x = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+                (lds_i32x2*)(lds + vb * LV::VBYTES + v8_base + 2 * c * LV::ROW + 32 * t));
+            f[2 * c] = x[0];
+            f[2 * c + 1] = x[1];
+          }
+          return f;
+        } else {
+          const int mt = t % NMT, u = t / NMT;
+          const u32x2 a0 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 0));
+          const u32x2 a1 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 1));
+          return u32x4{a0[0], a0[1], a1[0], a1[1]};
+        }
       };
 
-      u32x4 pb[4];
+      // P^T operands of GEMM-II: 16-bit, four fragments of 8 values (key step
+      // u = 16 keys); FP8, one fragment of all 32 of the lane's values, byte
+      // j = the score of key tile j / 16, register j % 16
+      Frag pb[FP8 ? 1 : 4];
+      // the pair of probabilities of chunk i (keys r0 and r0 + 1 of key tile
+      // kt = i / 8, r0 = 8 ((i / 4) % 2) + 2 (i % 4)) into the operand
+      auto put = [&](int i, float e0, float e1) __attribute__((always_inline)) {
+        const int u = i / 4, w = i % 4;
+        if constexpr (FP8) {
+          const int word = 2 * u + w / 2;
+          int32_t pk = (w % 2) ? Fp8::pack<true>(e0, e1, pb[0][word]) : Fp8::pack<false>(e0, e1, 0);
+          asm volatile("" : "+v"(pk));
+          pb[0][word] = pk;
+        } else {
+          uint32_t pk = Half<DT>::pack(e0, e1);
+          asm volatile("" : "+v"(pk));
+          pb[u][w] = pk;
+        }
+      };
       float lsum = 0.f;
       // one 16-bit pair of P^T (chunk i of 16): two FMAs, two exponentials, the
       // row-sum adds, one pack.  The row sum stays in fp32 (a sum of the
@@ -506,7 +607,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
         const int r0 = 8 * (u % 2) + 2 * w;
         const float e0 = __builtin_amdgcn_exp2f(fmaf(s[u / 2][r0], p.c, -mu));
         const float e1 = __builtin_amdgcn_exp2f(fmaf(s[u / 2][r0 + 1], p.c, -mu));
-        pb[u][w] = Half<DT>::pack(e0, e1);
+        put(i, e0, e1);
         lsum += e0 + e1;
       };
 
@@ -522,7 +623,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
       // live ranges.
       s_next[0] = f32x16{};
       s_next[1] = f32x16{};
-      u32x4 vring[AHEAD];
+      Frag vring[AHEAD];
       float xa[18], xb[18], ea[17], eb[17];
       float lsum_even = 0.f, lsum_odd = 0.f;
       auto arg = [&](int i, int k) __attribute__((always_inline)) {
@@ -542,9 +643,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
       for (int sidx = 0; sidx < NSLOT; ++sidx) {
         if ((sidx * NG1) % NSLOT == 0) {
           const int m = sidx * NG1 / NSLOT;   // MFMA m: k-step m / 2, key tile m % 2
-          const u32x4 a = kring[m % AHEAD];
+          const Frag a = kring[m % AHEAD];
           if (m + AHEAD < NG1) kring[m % AHEAD] = k_read(kb_next, (m + AHEAD) % 2, (m + AHEAD) / 2);
-          s_next[m % 2] = Half<DT>::mfma(a, qf[m / 2], s_next[m % 2]);
+          s_next[m % 2] = OP::mfma(a, qf[m / 2], s_next[m % 2]);
         }
         if (sidx >= NSLOT - AHEAD) vring[sidx - (NSLOT - AHEAD)] = v_frag(sidx - (NSLOT - AHEAD));
         // this block's direct loads, spread over the first half of the region
@@ -565,12 +666,10 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
         // 16-bit P^T operands; the row sum stays in fp32 (a sum of the rounded
         // values would carry their rounding into lse whenever a few keys
         // dominate the row)
-        // (the empty asm statement keeps the pack in this slot: left alone, the
-        // compiler sinks all 16 packs past the exact-path branch below, where
-        // no MFMA runs beside them)
-        uint32_t pk = Half<DT>::pack(ea[i], eb[i]);
-        asm volatile("" : "+v"(pk));
-        pb[i / 4][i % 4] = pk;
+        // (the empty asm statement in put keeps the pack in this slot: left
+        // alone, the compiler sinks all 16 packs past the exact-path branch
+        // below, where no MFMA runs beside them)
+        put(i, ea[i], eb[i]);
         if (i % 2 == 0) lsum_even += ea[i] + eb[i];
         else lsum_odd += ea[i] + eb[i];
         __builtin_amdgcn_sched_barrier(0);
@@ -580,6 +679,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
 
       // exact path (rare): the running maximum rises
       if (__any(lsum > kPmax)) {
+        // a use of GEMM-I's results on this path too keeps the compiler from
+        // sinking GEMM-I's MFMAs out of region 1 to past this branch
+        asm volatile("" :: "v"(s_next[0]), "v"(s_next[1]));
         const float m_blk = row_max(s) * p.c;
         const float m_new = fmaxf(m_run, m_blk);
         const float alpha = (m_run == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
@@ -597,9 +699,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
       // Straight-line region 2: GEMM-II, O^T += V^T P^T
   #pragma unroll
       for (int t = 0; t < NV; ++t) {
-        const u32x4 a = vring[t % AHEAD];
+        const Frag a = vring[t % AHEAD];
         if (t + AHEAD < NV) vring[t % AHEAD] = v_frag(t + AHEAD);
-        oacc[t % NMT] = Half<DT>::mfma(a, pb[t / NMT], oacc[t % NMT]);
+        oacc[t % NMT] = OP::mfma(a, pb[FP8 ? 0 : t / NMT], oacc[t % NMT]);
         __builtin_amdgcn_sched_barrier(0);
       }
     };
@@ -659,14 +761,16 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
 
     // ---- epilogue: O = O / l in the storage type, lse in natural log ----
     const float l_tot = sum_across_halves(l_run);
-    const float inv = 1.0f / l_tot;
-    const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.o + (size_t)bh * N * DV, head_bytes_v);
+    const float inv = p.vscale / l_tot;
+    // the output is 16-bit for every input type (FP8 inputs give bf16)
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.o + (size_t)bh * N * DV, (uint32_t)N * DV * 2);
   #pragma unroll
     for (int mt = 0; mt < NMT; ++mt) {
   #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const u32x2 w = {Half<DT>::pack(oacc[mt][4 * g] * inv, oacc[mt][4 * g + 1] * inv),
-                         Half<DT>::pack(oacc[mt][4 * g + 2] * inv, oacc[mt][4 * g + 3] * inv)};
+        using OutT = Half<FP8 ? 1 : DT>;   // FP8 inputs give a bf16 output
+        const u32x2 w = {OutT::pack(oacc[mt][4 * g] * inv, oacc[mt][4 * g + 1] * inv),
+                         OutT::pack(oacc[mt][4 * g + 2] * inv, oacc[mt][4 * g + 3] * inv)};
         __builtin_amdgcn_raw_buffer_store_b64(w, ro, (uint32_t)(qrow * DV + 32 * mt + 8 * g + 4 * hi) * 2, 0, 0);
       }
     }
@@ -683,7 +787,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
 template <int DK, int DV, int DT, bool CAUSAL>
 hipError_t launch_instance(const KParams& kp, hipStream_t stream) {
   auto kern = attn_fwd_kernel<DK, DV, DT, CAUSAL>;
-  constexpr size_t lds = lds_bytes<DK, DV>();
+  constexpr size_t lds = lds_bytes<DK, DV, DT>();
   static_assert(lds <= 160 * 1024, "one workgroup's LDS fits a CU");
   static const hipError_t attr = hipFuncSetAttribute(
       reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -696,9 +800,9 @@ hipError_t launch_instance(const KParams& kp, hipStream_t stream) {
 
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
   KParams kp;
-  kp.q = a.q;
-  kp.k = a.k;
-  kp.v = a.v;
+  kp.q = static_cast<const uint8_t*>(a.q);
+  kp.k = static_cast<const uint8_t*>(a.k);
+  kp.v = static_cast<const uint8_t*>(a.v);
   kp.o = a.o;
   kp.lse = a.lse;
   kp.N = a.N;
@@ -709,10 +813,11 @@ hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
   kp.wg_per_head = a.causal ? (kp.nq + 1) / 2 : kp.nq;
   kp.total = kp.wg_per_head * a.B * a.H;
   kp.c = a.c;
+  kp.vscale = a.vscale;
   kp.qmode = a.qmode;
-  // head dimensions (d_qk, d_v): 64/64, 128/128, 192/128
+  // head dimensions (d_qk, d_v): 64/64, 128/128, 192/128; FP8: 128/128
   const int dims = a.d == 64 ? 0 : (a.d == 128 ? 1 : 2);
-  const int key = dims * 4 + a.dtype * 2 + a.causal;
+  const int key = a.dtype == 2 ? 12 + a.causal : dims * 4 + a.dtype * 2 + a.causal;
   switch (key) {
     case 0: return launch_instance<64, 64, 0, false>(kp, stream);
     case 1: return launch_instance<64, 64, 0, true>(kp, stream);
@@ -726,6 +831,8 @@ hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
     case 9: return launch_instance<192, 128, 0, true>(kp, stream);
     case 10: return launch_instance<192, 128, 1, false>(kp, stream);
     case 11: return launch_instance<192, 128, 1, true>(kp, stream);
+    case 12: return launch_instance<128, 128, 2, false>(kp, stream);
+    case 13: return launch_instance<128, 128, 2, true>(kp, stream);
   }
   return hipErrorInvalidValue;
 }

@@ -17,17 +17,18 @@ namespace qm {
 enum QMode : int { kQNormal = 0, kQNegate = 1, kQZero = 2 };
 
 struct AttnArgs {
-  const uint16_t* q;
-  const uint16_t* k;
-  const uint16_t* v;
+  const void* q;       // 16-bit or FP8 (one byte) elements
+  const void* k;
+  const void* v;
   uint16_t* o;
   float* lse;
   int B, H, N, d;  // d: head dimension of q and k (d_qk)
   int dv;         // head dimension of v and o: d, or 128 when d = 192
   int Hkv;      // key/value heads; H % Hkv == 0, query head h reads h / (H / Hkv)
   int causal;   // 0 or 1
-  int dtype;    // 0 = fp16, 1 = bf16
-  float c;      // |scale| * log2(e), a normal positive float
+  int dtype;    // 0 = fp16, 1 = bf16, 2 = FP8 E4M3 inputs with a bf16 output
+  float c;      // |scale| * log2(e) (FP8: |scale * q_scale * k_scale| * log2(e)), normal, > 0
+  float vscale; // factor applied to O: 1, or the FP8 value scale
   int qmode;    // QMode
 };
 

@@ -28,16 +28,20 @@ bool finite_bits(float x) {
   return (u & 0x7F800000u) != 0x7F800000u;
 }
 
+constexpr int kFp8 = 2;   // internal dtype code: FP8 E4M3 inputs, bf16 output
+
 // Validation and dispatch shared by the entry points: H query heads read Hkv
 // key/value heads (Hkv == H for plain multi-head attention); q and k have head
-// dimension d, v and o head dimension dv.
+// dimension d, v and o head dimension dv.  dtype kFp8: q, k, v hold one-byte
+// E4M3 codes scaled by qs, ks, vs, and o is bf16.
 int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H,
              int Hkv, int N, int d, int dv, float scale, int causal, hipStream_t stream,
-             int dtype) {
+             int dtype, float qs = 1.0f, float ks = 1.0f, float vs = 1.0f) {
   if (!q || !k || !v || !o || !lse) return QM_ERR_NULL;
   if (B < 1 || H < 1 || N < 1 || Hkv < 1 || Hkv > H || H % Hkv != 0) return QM_ERR_SHAPE;
   if (!((d == 64 && dv == 64) || (d == 128 && dv == 128) || (d == 192 && dv == 128)))
     return QM_ERR_HEADDIM;
+  if (dtype == kFp8 && !(d == 128 && dv == 128)) return QM_ERR_HEADDIM;
   // element counts: the whole tensor in 62 bits, one head's [N][d] slab and the
   // workgroup count in 31 bits (the kernels index within a head in 32 bits)
   const uint64_t bh = (uint64_t)B * (uint64_t)H;
@@ -49,13 +53,15 @@ int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, i
   if ((uint64_t)(N + 256) * (uint64_t)d >= (1ull << 31) || bh >= (1ull << 62) / nd)
     return QM_ERR_SHAPE;
   if ((uint64_t)((N + 255) / 256) * bh > (uint64_t)INT_MAX) return QM_ERR_SHAPE;
-  if (dtype != QM_F16 && dtype != QM_BF16) return QM_ERR_DTYPE;
-  if (!finite_bits(scale)) return QM_ERR_SCALE;
+  if (dtype != QM_F16 && dtype != QM_BF16 && dtype != kFp8) return QM_ERR_DTYPE;
+  if (!finite_bits(scale) || !finite_bits(qs) || !finite_bits(ks) || !finite_bits(vs))
+    return QM_ERR_SCALE;
   if (causal != 0 && causal != 1) return QM_ERR_CAUSAL;
 
-  const size_t q_bytes = (size_t)(bh * nd) * 2;
-  const size_t k_bytes = (size_t)(bhkv * nd) * 2;
-  const size_t v_bytes = (size_t)(bhkv * ndv) * 2;
+  const size_t es = dtype == kFp8 ? 1 : 2;   // bytes per q, k, v element
+  const size_t q_bytes = (size_t)(bh * nd) * es;
+  const size_t k_bytes = (size_t)(bhkv * nd) * es;
+  const size_t v_bytes = (size_t)(bhkv * ndv) * es;
   const size_t o_bytes = (size_t)(bh * ndv) * 2;
   const size_t lse_bytes = (size_t)(bh * (uint64_t)N) * sizeof(float);
   if (overlaps(o, o_bytes, q, q_bytes) || overlaps(o, o_bytes, k, k_bytes) ||
@@ -67,9 +73,9 @@ int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, i
     return QM_ERR_UNSUPPORTED;
 
   qm::AttnArgs a;
-  a.q = static_cast<const uint16_t*>(q);
-  a.k = static_cast<const uint16_t*>(k);
-  a.v = static_cast<const uint16_t*>(v);
+  a.q = q;
+  a.k = k;
+  a.v = v;
   a.o = static_cast<uint16_t*>(o);
   a.lse = lse;
   a.B = B;
@@ -80,15 +86,22 @@ int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, i
   a.dv = dv;
   a.causal = causal;
   a.dtype = dtype;
-  // exp2-domain scale; the sign goes into Q (exact), a zero or negligible
-  // scale becomes all-zero scores (exact: every visible score is 0)
-  const double c = fabs((double)scale) * 1.4426950408889634074;
+  a.vscale = vs;
+  // exp2-domain scale of the stored codes' dot product (FP8: times the q and k
+  // scales); the sign goes into Q (exact), a zero or negligible scale becomes
+  // all-zero scores (exact: every visible score is 0)
+  const double qk = (double)scale * (double)qs * (double)ks;
+  const double c = fabs(qk) * 1.4426950408889634074;
   a.c = (float)c;
-  if (!(a.c >= FLT_MIN)) {
-    a.c = 1.0f;
-    a.qmode = qm::kQZero;
+  if (!(a.c >= FLT_MIN) || !(c < (double)FLT_MAX)) {
+    if (!(a.c >= FLT_MIN)) {
+      a.c = 1.0f;
+      a.qmode = qm::kQZero;
+    } else {
+      return QM_ERR_SCALE;   // the combined scale overflows fp32
+    }
   } else {
-    a.qmode = scale < 0.0f ? qm::kQNegate : qm::kQNormal;
+    a.qmode = qk < 0.0 ? qm::kQNegate : qm::kQNormal;
   }
   return qm::launch_attn_fwd(a, stream) == hipSuccess ? QM_OK : QM_ERR_LAUNCH;
 }
@@ -98,19 +111,30 @@ int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, i
 extern "C" int qm_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
                            int B, int H, int N, int d, float scale, int causal,
                            hipStream_t stream, int dtype) {
-  return attn_fwd(q, k, v, o, lse, B, H, H, N, d, d, scale, causal, stream, dtype);
+  return attn_fwd(q, k, v, o, lse, B, H, H, N, d, d, scale, causal, stream,
+                  dtype == kFp8 ? -1 : dtype);   // FP8 has its own entry point
 }
 
 extern "C" int qm_attn_fwd_gqa(const void* q, const void* k, const void* v, void* o,
                                float* lse, int B, int H, int Hkv, int N, int d, float scale,
                                int causal, hipStream_t stream, int dtype) {
-  return attn_fwd(q, k, v, o, lse, B, H, Hkv, N, d, d, scale, causal, stream, dtype);
+  return attn_fwd(q, k, v, o, lse, B, H, Hkv, N, d, d, scale, causal, stream,
+                  dtype == kFp8 ? -1 : dtype);   // FP8 has its own entry point
+}
+
+extern "C" int qm_attn_fwd_fp8(const void* q, const void* k, const void* v, void* o,
+                               float* lse, int B, int H, int N, int d, float q_scale,
+                               float k_scale, float v_scale, float scale, int causal,
+                               hipStream_t stream) {
+  return attn_fwd(q, k, v, o, lse, B, H, H, N, d, d, scale, causal, stream, kFp8, q_scale,
+                  k_scale, v_scale);
 }
 
 extern "C" int qm_attn_fwd_mla(const void* q, const void* k, const void* v, void* o,
                                float* lse, int B, int H, int N, int d_qk, int d_v, float scale,
                                int causal, hipStream_t stream, int dtype) {
-  return attn_fwd(q, k, v, o, lse, B, H, H, N, d_qk, d_v, scale, causal, stream, dtype);
+  return attn_fwd(q, k, v, o, lse, B, H, H, N, d_qk, d_v, scale, causal, stream,
+                  dtype == kFp8 ? -1 : dtype);   // FP8 has its own entry point
 }
 
 extern "C" const char* qm_attn_strerror(int status) {
@@ -120,9 +144,9 @@ extern "C" const char* qm_attn_strerror(int status) {
     case QM_ERR_SHAPE:
       return "B, H or N is below 1, Hkv does not divide H, or the tensors are too large";
     case QM_ERR_HEADDIM:
-      return "head dimensions must be 64 or 128 (or d_qk = 192 with d_v = 128)";
+      return "head dimensions must be 64 or 128 (or d_qk = 192 with d_v = 128; FP8: 128)";
     case QM_ERR_DTYPE: return "dtype must be QM_F16 (0) or QM_BF16 (1)";
-    case QM_ERR_SCALE: return "scale must be finite";
+    case QM_ERR_SCALE: return "scale (and the FP8 tensor scales) must be finite";
     case QM_ERR_ALIAS: return "o or lse overlaps an input or each other";
     case QM_ERR_CAUSAL: return "causal must be 0 or 1";
     case QM_ERR_LAUNCH: return "the HIP runtime rejected the kernel launch";

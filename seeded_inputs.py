@@ -76,27 +76,32 @@ def make_qkv(B: int, H: int, N: int, d: int, dtype: str, seed: int = 0,
 
 # ---------------------------------------------------------------- FP8 inputs
 # OCP E4M3FN: 1 sign, 4 exponent (bias 7) and 3 mantissa bits; no infinities;
-# S.1111.111 is NaN; the largest finite value is 448.  Non-negative finite
-# values in code order, for nearest-value rounding below.
-_E4M3_POS = np.array([(c & 7) / 8 * 2.0 ** -6 if (c >> 3) == 0 else
-                      (1 + (c & 7) / 8) * 2.0 ** ((c >> 3) - 7) for c in range(127)])
+# S.1111.111 is NaN; the largest finite value is 448.
 E4M3_MAX = 448.0
 
 
 def f32_to_e4m3_bits(x: np.ndarray) -> np.ndarray:
-    """Round finite values with |x| <= 448 to OCP E4M3FN, to nearest with ties
-    to the even code (the even mantissa); return the uint8 codes."""
-    x = np.asarray(x, dtype=np.float64)
-    a = np.abs(x)
-    if not np.all(a <= E4M3_MAX):
+    """Round finite fp32 values with |x| <= 448 to OCP E4M3FN, to nearest with
+    ties to the even code (the even mantissa); return the uint8 codes.
+
+    Normal results (|x| >= 2^-6): round the fp32 significand to 3 bits on the
+    bit pattern; the code is then (exponent + 7) << 3 | mantissa.  Subnormal
+    results: the code is |x| / 2^-9 rounded half to even (8 there is 2^-6,
+    which is code 8 as well)."""
+    x = np.asarray(x)
+    x32 = np.ascontiguousarray(x, dtype=np.float32)
+    if x.dtype != np.float32 and not np.array_equal(x32, x):
+        raise ValueError("inputs must be fp32 values")
+    a = np.abs(x32)
+    if not np.all(a <= np.float32(E4M3_MAX)):
         raise ValueError("values beyond the E4M3 range (448) or NaN")
-    hi = np.clip(np.searchsorted(_E4M3_POS, a, side="left"), 0, 126)   # first value >= a
-    lo = np.clip(hi - 1, 0, 126)
-    dlo = a - _E4M3_POS[lo]
-    dhi = _E4M3_POS[hi] - a
-    take_hi = (dhi < dlo) | ((dhi == dlo) & (hi % 2 == 0))
-    code = np.where(take_hi, hi, lo).astype(np.uint8)
-    return np.where(np.signbit(x), code | 0x80, code).astype(np.uint8)   # keeps -0
+    u = a.view(np.uint32)
+    lsb = (u >> np.uint32(20)) & np.uint32(1)
+    r = (u + np.uint32(0x7FFFF) + lsb) >> np.uint32(20)          # sign 0, 8-bit exponent, 3 bits
+    normal = (((r >> np.uint32(3)).astype(np.int32) - 127 + 7) << 3) | (r & np.uint32(7)).astype(np.int32)
+    sub = np.rint(a * np.float32(512.0)).astype(np.int32)
+    code = np.where(a >= np.float32(2.0 ** -6), normal, sub).astype(np.uint8)
+    return np.where(np.signbit(x32), code | np.uint8(0x80), code).astype(np.uint8)   # keeps -0
 
 
 def make_qkv_fp8(B: int, H: int, N: int, d: int, seed: int = 0):
@@ -114,6 +119,30 @@ def make_qkv_fp8(B: int, H: int, N: int, d: int, seed: int = 0):
         scales.append(float(s))
         del x, y
     return out[0], out[1], out[2], tuple(scales)
+
+
+def make_qkv_fp8_dyadic(B: int, H: int, N: int, d: int, seed: int = 0,
+                        v_binade: bool = False):
+    """FP8 inputs with small integer dot products.  Each Q row holds +1 or -1
+    (even odds) at two distinct columns drawn uniformly and zeros elsewhere; K
+    entries are integers drawn uniformly from -2 .. 2; V holds codes drawn
+    uniformly from the 254 finite E4M3 codes (every exponent, subnormals and
+    both zeros included), or with ``v_binade`` from the 16 codes of [1, 2)
+    and (-2, -1] (random sign and mantissa).  Every q . k is then an integer
+    in [-4, 4].  Returns uint8 codes (q8, k8, v8); the caller picks the scale
+    factors."""
+    rng = np.random.default_rng(seed)
+    cols = np.argsort(rng.random((B, H, N, d)), axis=-1)[..., :2]
+    signs = rng.choice(np.array([-1.0, 1.0], dtype=np.float32), size=(B, H, N, 2))
+    q = np.zeros((B, H, N, d), dtype=np.float32)
+    np.put_along_axis(q, cols, signs, axis=-1)
+    k = rng.integers(-2, 3, size=(B, H, N, d)).astype(np.float32)
+    if v_binade:
+        pool = np.array([s << 7 | 7 << 3 | m for s in (0, 1) for m in range(8)], dtype=np.uint8)
+    else:
+        pool = np.array([c for c in range(256) if c & 0x7F != 0x7F], dtype=np.uint8)
+    v = pool[rng.integers(0, pool.size, size=(B, H, N, d))]
+    return f32_to_e4m3_bits(q), f32_to_e4m3_bits(k), v
 
 
 def default_scale(d: int) -> float:

@@ -37,7 +37,7 @@ def _declared_functions():
 
 
 def test_header_declares_entry_points():
-    assert {"qm_attn_fwd", "qm_attn_fwd_gqa", "qm_attn_fwd_mla",
+    assert {"qm_attn_fwd", "qm_attn_fwd_gqa", "qm_attn_fwd_mla", "qm_attn_fwd_fp8",
             "qm_attn_strerror"} <= set(_declared_functions())
 
 
@@ -172,6 +172,42 @@ def test_mla_invalid_arguments_are_rejected(lib, d_qk, d_v, over, status):
 
 def test_plain_entry_rejects_the_mla_head(lib):
     assert call(d=192) == qa.QM_ERR_HEADDIM
+
+
+def call_fp8(qs=0.01, ks=0.01, vs=0.01, **over):
+    a = dict(GOOD)
+    a.update(over)
+    return qa.qm_attn_fwd_fp8(a["q"], a["k"], a["v"], a["o"], a["lse"], a["B"], a["H"], a["N"],
+                              a["d"], qs, ks, vs, a["scale"], a["causal"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(d=64), qa.QM_ERR_HEADDIM),                    # FP8 runs at d = 128 only
+    (dict(d=192), qa.QM_ERR_HEADDIM),
+    (dict(d=128, q=None), qa.QM_ERR_NULL),
+    (dict(d=128, N=0), qa.QM_ERR_SHAPE),
+    (dict(d=128, qs=float("inf")), qa.QM_ERR_SCALE),
+    (dict(d=128, ks=float("nan")), qa.QM_ERR_SCALE),
+    (dict(d=128, vs=float("-inf")), qa.QM_ERR_SCALE),
+    (dict(d=128, scale=float("nan")), qa.QM_ERR_SCALE),
+    (dict(d=128, qs=3e38, ks=3e38, lse=L + 4), qa.QM_ERR_UNSUPPORTED),   # alignment comes first
+    (dict(d=128, qs=3e38, ks=3e38), qa.QM_ERR_SCALE),    # the combined scale overflows
+    (dict(d=128, causal=2), qa.QM_ERR_CAUSAL),
+    # B=1, H=2, N=128, d=128: q, k, v span 32 KiB of one-byte codes, o 64 KiB of bf16
+    (dict(d=128, o=Q + 16 * 1024), qa.QM_ERR_ALIAS),
+    (dict(d=128, lse=V + 8 * 1024), qa.QM_ERR_ALIAS),
+    (dict(d=128, k=K + 8), qa.QM_ERR_UNSUPPORTED),
+], ids=lambda x: str(x))
+def test_fp8_invalid_arguments_are_rejected(lib, kw, status):
+    kw = dict(kw)
+    qs, ks, vs = kw.pop("qs", 0.01), kw.pop("ks", 0.01), kw.pop("vs", 0.01)
+    assert call_fp8(qs, ks, vs, **kw) == status
+
+
+def test_16bit_entries_reject_the_fp8_code(lib):
+    assert call(dtype=2) == qa.QM_ERR_DTYPE
+    assert call_gqa(1, H=2, dtype=2) == qa.QM_ERR_DTYPE
+    assert call_mla(128, 128, dtype=2) == qa.QM_ERR_DTYPE
 
 
 def test_inputs_may_alias_each_other(lib):

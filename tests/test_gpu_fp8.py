@@ -1,0 +1,261 @@
+"""GPU parity for the FP8 forward (``qm_attn_fwd_fp8``): OCP E4M3 inputs with
+per-tensor scale factors, bf16 output, head dimension 128.
+
+Two roundings separate the kernel from the exact definition on general
+inputs.
+
+* P is rounded to E4M3 for the P.V product: relative error at most 2^-4 for a
+  normal value, absolute at most 2^-10 (half the subnormal spacing 2^-9) in
+  units of the largest weight, since the weights are formed against a running
+  maximum no larger than the row's true maximum.
+* The FP8 matrix-core instruction sums its 64 products in groups of 8
+  consecutive k: within a group every product is truncated toward zero to a
+  multiple of 2^(E - 13), E the exponent of the group's largest product, and
+  the group sums enter the fp32 accumulator (measured on gfx950 with one-hot
+  operands).  A group of 8 thus loses less than 7 x 2^-13 of its largest
+  product.  On the scores this is an absolute error of at most
+  Delta_i = 7 x 2^-13 |scale q_scale k_scale| max_j sum_c |q_ic k_jc| (plus
+  fp32 rounding), which moves each normalised weight by a factor within
+  exp(+-2 Delta_i); on P.V it is at most 7 x 2^-13 of sum_j P_ij |v_jc|.
+
+Per output element (row i, column c), with P the exact softmax weights and v
+the real (scaled) values:
+
+    |O - O_ref| <= ((1 + 2^-4) e^(2 Delta_i) (1 + 7 x 2^-13) - 1) sum_j P_ij |v_jc|
+                   + 2^-10 e^(2 Delta_i) max_j P_ij sum_j |v_jc|
+                   + half a bf16 ulp + fp32 summation terms.
+
+That bound is loose for a layout test, so most cases use inputs on which no
+rounding happens: integer scores in [-4, 4] and a combined softmax scale of
+ln 2 make every weight a power of two between 2^-8 and 2^8 (relative to any
+maximum the kernel may hold), all exact in E4M3; Q.K products are small
+integers, which no group truncates; with V in one binade the P.V products of
+a group span less than 2^10, so their truncation drops nothing either.
+There the kernel must match the oracle to fp32 summation error and the bf16
+output rounding.  With V over all E4M3 codes only the P.V group truncation
+is added.  Independently of the oracle, the FP8 kernel must agree with the
+bf16 kernel on the same real values when neither rounds.
+"""
+from __future__ import annotations
+
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import seeded_inputs as si
+from oracle import (attention_fp64, attention_rows_fp64, decode_fp64, scores_fp64,
+                    softmax_rows_fp64)
+from tests.gpu_util import LSE_TOL, half_ulp, to_host64
+
+pytestmark = pytest.mark.gpu
+
+LN2 = math.log(2.0)
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def qa():
+    import torch
+    import paper_2506_12355_amd as qa
+    assert torch.cuda.is_available()
+    qa.load_library()
+    return qa
+
+
+def _codes(x):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x)).cuda().view(torch.float8_e4m3fn)
+
+
+def _run(qa, q8, k8, v8, scales, causal, scale):
+    import torch
+    o, lse = qa.fwd_fp8(_codes(q8), _codes(k8), _codes(v8), scales, causal=causal, scale=scale)
+    torch.cuda.synchronize()
+    return to_host64(o), to_host64(lse)
+
+
+def _gate(O, lse, Or, lr, bound, what):
+    assert O.shape == Or.shape, (O.shape, Or.shape)
+    assert np.all(np.isfinite(O)) and np.all(np.isfinite(lse)), f"{what}: non-finite output"
+    err = np.abs(O - Or)
+    bad = err > bound
+    if np.any(bad):
+        idx = np.unravel_index(np.argmax(err - bound), err.shape)
+        raise AssertionError(
+            f"{what}: {int(bad.sum())} O elements outside the gate; worst at {idx}: "
+            f"gpu={O[idx]!r} ref={Or[idx]!r} err={err[idx]:.3e} bound={bound[idx]:.3e}")
+    lerr = np.abs(lse - lr)
+    assert lerr.max() <= LSE_TOL, f"{what}: lse err {lerr.max():.3e}"
+    return float(err.max()), float(lerr.max())
+
+
+def _summation(N):
+    """Relative fp32 error allowance of the two length-N sums (O and l)."""
+    return 2 * (N + 128) * 2.0 ** -24 + 1e-5
+
+
+GROUP_TRUNC = 7 * 2.0 ** -13   # the matrix core's in-group truncation, relative
+
+
+def _tight_case(qa, q8, k8, v8, scales, causal, scale, what, pv_trunc=False):
+    """Exact-weight inputs: the oracle's value up to fp32 summation and the
+    bf16 output rounding (plus, with ``pv_trunc``, the P.V group truncation)."""
+    _say(f"case {what}: shape={q8.shape} scales={scales} scale={scale} causal={causal}")
+    O, lse = _run(qa, q8, k8, v8, scales, causal, scale)
+    Or, lr = attention_fp64(q8, k8, v8, scale, causal, "e4m3", descale=scales)
+    PV, _ = attention_fp64(q8, k8, v8 & 0x7F, scale, causal, "e4m3", descale=scales)
+    N = q8.shape[2]
+    rel = _summation(N) + (GROUP_TRUNC if pv_trunc else 0.0)
+    bound = np.maximum(half_ulp(Or, "bf16"), half_ulp(O, "bf16")) + rel * PV
+    return _gate(O, lse, Or, lr, bound, what)
+
+
+# -------------------------------------------------- exact-rounding inputs
+@pytest.mark.parametrize("scales,scale", [
+    ((0.5, 2.0, 0.0123), LN2),            # q_scale * k_scale = 1
+    ((0.25, 2.0, 1.0), 2 * LN2),          # q_scale * k_scale = 1/2
+    ((1.0, 1.0, 3.5), -LN2),              # negative scale: the kernel flips Q's signs
+])
+def test_dyadic_inputs_full(qa, scales, scale):
+    q8, k8, v8 = si.make_qkv_fp8_dyadic(2, 3, 333, 128, seed=11, v_binade=True)
+    for causal in (False, True):
+        _tight_case(qa, q8, k8, v8, scales, causal, scale, f"dyadic scales={scales}")
+
+
+def test_dyadic_inputs_all_value_codes(qa):
+    """Every E4M3 code in V (subnormals, both zeros, 448): the decode of V is
+    exact, only the matrix core's in-group truncation of P.V is allowed."""
+    q8, k8, v8 = si.make_qkv_fp8_dyadic(2, 3, 333, 128, seed=11)
+    for causal in (False, True):
+        _tight_case(qa, q8, k8, v8, (0.5, 2.0, 0.0123), causal, LN2, "dyadic, all V codes",
+                    pv_trunc=True)
+
+
+@pytest.mark.parametrize("N", [1, 2, 63, 64, 65, 129, 255, 1000, 2111])
+def test_dyadic_edge_lengths(qa, N):
+    q8, k8, v8 = si.make_qkv_fp8_dyadic(1, 2, N, 128, seed=N, v_binade=True)
+    for causal in (False, True):
+        _tight_case(qa, q8, k8, v8, (1.0, 1.0, 0.01), causal, LN2, f"dyadic N={N}")
+
+
+def test_negligible_scores_give_uniform_weights(qa):
+    """A combined score scale too small to change any score: every visible key
+    weighs the same (the kernel zeroes Q; the oracle's scores are ~1e-60)."""
+    q8, k8, v8 = si.make_qkv_fp8_dyadic(1, 2, 300, 128, seed=5, v_binade=True)
+    for causal in (False, True):
+        _tight_case(qa, q8, k8, v8, (1e-30, 1e-30, 0.25), causal, 0.088,
+                    f"negligible scores causal={causal}")
+
+
+def test_fp8_agrees_with_bf16_kernel(qa):
+    """Same real values through both kernels: Q = +-1/2 and K = 2 x integers
+    (exact in bf16), V = 2^-6 x one-binade E4M3 values (exact in bf16), and
+    power-of-two weights that neither kernel rounds.  Only the fp32 summation
+    order and the output rounding may differ."""
+    import torch
+    q8, k8, v8 = si.make_qkv_fp8_dyadic(2, 4, 700, 128, seed=21, v_binade=True)
+    scales = (0.5, 2.0, 2.0 ** -6)
+    for causal in (False, True):
+        _say(f"case fp8 vs bf16 causal={causal}")
+        O8, l8 = _run(qa, q8, k8, v8, scales, causal, LN2)
+        real = [torch.from_numpy(decode_fp64(x, "e4m3") * s).to(torch.bfloat16).cuda()
+                for x, s in zip((q8, k8, v8), scales)]
+        for t, x, s in zip(real, (q8, k8, v8), scales):
+            assert np.array_equal(t.double().cpu().numpy(), decode_fp64(x, "e4m3") * s)
+        o16, l16 = qa.fwd(*real, causal=causal, scale=LN2)
+        torch.cuda.synchronize()
+        O16, L16 = to_host64(o16), to_host64(l16)
+        PV, _ = attention_fp64(q8, k8, v8 & 0x7F, LN2, causal, "e4m3", descale=scales)
+        bound = (np.maximum(half_ulp(O8, "bf16"), half_ulp(O16, "bf16")) * 2
+                 + 2 * _summation(700) * PV)
+        _gate(O8, l8, O16, L16, bound, f"fp8 vs bf16 causal={causal}")
+
+
+# -------------------------------------------------- general FP8 inputs
+def _rounding_bound(q8, k8, v8, scales, scale, causal, rows, O, Or):
+    """The general-input bound of the module docstring, per sampled row and
+    column, from the oracle's own scores and weights."""
+    sq, sk, sv = (float(np.float32(s)) for s in scales)
+    scale64 = float(np.float32(scale))
+    cnat = abs(scale64 * sq * sk)
+    bound = np.empty_like(Or)
+    heads = {}
+    for idx, (b, h, i) in enumerate(rows):
+        if (b, h) not in heads:
+            K8 = decode_fp64(k8[b, h], "e4m3")
+            heads = {(b, h): (K8 * sk, np.abs(K8), np.abs(decode_fp64(v8[b, h], "e4m3")) * sv)}
+        K, Ka, Va = heads[(b, h)]
+        Q8 = decode_fp64(q8[b, h, i:i + 1], "e4m3")
+        S = scores_fp64(Q8 * sq, K, scale64, causal, row0=i)
+        P, _ = softmax_rows_fp64(S)
+        vis = np.isfinite(S[0])
+        # largest sum of |q_c k_c| over the visible keys: the scores' truncation
+        delta = (GROUP_TRUNC + 2.0 ** -20) * cnat * float((np.abs(Q8) @ Ka[vis].T).max())
+        grow = np.exp(2 * delta)
+        pv = P[0] @ Va
+        rel = (1 + 2.0 ** -4) * grow * (1 + GROUP_TRUNC) - 1 + _summation(K.shape[0])
+        bound[idx] = rel * pv + 2.0 ** -10 * grow * P.max() * Va[vis].sum(axis=0)
+    return bound + np.maximum(half_ulp(Or, "bf16"), half_ulp(O, "bf16"))
+
+
+def test_small_fp8_workload_full(qa):
+    w = si.WORKLOADS["fp8_b2_h3_n333_d128"]
+    q8, k8, v8, scales = w.fp8_inputs()
+    rows = [(b, h, i) for b in range(w.B) for h in range(w.H) for i in range(w.N)]
+    for causal in w.causal:
+        _say(f"case {w.name} causal={causal}")
+        O, lse = _run(qa, q8, k8, v8, scales, causal, w.scale)
+        Or, lr = attention_fp64(q8, k8, v8, w.scale, causal, "e4m3", descale=scales)
+        Of, Orf = O.reshape(-1, w.d), Or.reshape(-1, w.d)
+        bound = _rounding_bound(q8, k8, v8, scales, w.scale, causal, rows, Of, Orf)
+        err, _ = _gate(Of, lse.ravel(), Orf, lr.ravel(), bound, f"{w.name} causal={causal}")
+        # the bound is worst case; rounding errors of independent weights mostly
+        # cancel, so the typical error sits far below it
+        rms = float(np.sqrt(np.mean((Of - Orf) ** 2)))
+        assert rms < 0.1 * float(np.sqrt(np.mean(bound ** 2))), rms
+
+
+def _sample_rows(w, n, seed):
+    rng = np.random.default_rng(seed)
+    fixed = [0, 1, 63, 64, 255, 256, w.N // 2, w.N - 257, w.N - 2, w.N - 1]
+    return [(int(rng.integers(w.B)), int(rng.integers(w.H)),
+             fixed[t] if t < len(fixed) else int(rng.integers(w.N))) for t in range(n)]
+
+
+@pytest.fixture(scope="module")
+def long_inputs():
+    w = si.WORKLOADS["fp8_b2_h32_n8192_d128"]
+    _say(f"drawing the inputs of {w.name}")
+    return w, w.fp8_inputs()
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_long_fp8_workload_sampled(qa, long_inputs, causal):
+    """The FP8 benchmark workload (B = 2, H = 32, N = 8192, d = 128) in the
+    launch configuration the benchmark times, on sampled rows."""
+    import torch
+    w, (q8, k8, v8, scales) = long_inputs
+    tq, tk, tv = _codes(q8), _codes(k8), _codes(v8)
+    _say(f"case {w.name} causal={causal}: running")
+    o, lse = qa.fwd_fp8(tq, tk, tv, scales, causal=causal, scale=w.scale)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(o).all()) and bool(torch.isfinite(lse).all())
+    vmax = 448.0 * float(np.float32(scales[2]))
+    # a convex combination of the values, up to the weights' E4M3 rounding
+    assert float(o.abs().float().max()) <= vmax * 1.125
+    # the inputs are read only
+    assert torch.equal(tq.view(torch.uint8).cpu(), torch.from_numpy(q8))
+    assert torch.equal(tv.view(torch.uint8).cpu(), torch.from_numpy(v8))
+    rows = sorted(_sample_rows(w, 96, seed=8 + causal))
+    ix = tuple(torch.tensor(np.array(rows).T).cuda())
+    O, L = to_host64(o[ix]), to_host64(lse[ix])
+    _say(f"case {w.name} causal={causal}: oracle on {len(rows)} rows")
+    Or, lr = attention_rows_fp64(q8, k8, v8, w.scale, causal, "e4m3", rows, descale=scales)
+    bound = _rounding_bound(q8, k8, v8, scales, w.scale, causal, rows, O, Or)
+    _gate(O, L, Or, lr, bound, f"{w.name} causal={causal} sampled rows")

@@ -67,6 +67,11 @@ def test_e4m3_rounding_matches_the_library():
     assert np.array_equal(mine, ref)
     with pytest.raises(ValueError):
         si.f32_to_e4m3_bits(np.array([500.0]))
+    # a strided sweep over every fp32 bit pattern up to 448, both signs
+    u = np.arange(0, 0x43E00001, 97, dtype=np.uint32)
+    x = np.concatenate([u, u | np.uint32(0x80000000)]).view(np.float32)
+    ref = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    assert np.array_equal(si.f32_to_e4m3_bits(x), ref)
 
 
 def test_fp8_inputs_use_the_full_range():
@@ -79,3 +84,23 @@ def test_fp8_inputs_use_the_full_range():
     rng = np.random.default_rng(3)
     x = rng.standard_normal((2, 3, 50, 16), dtype=np.float32)
     assert np.float32(np.max(np.abs(x)) / np.float32(448.0)) == np.float32(sc[0])
+
+
+def test_dyadic_fp8_inputs_have_small_integer_scores():
+    torch = pytest.importorskip("torch")
+    q8, k8, v8 = si.make_qkv_fp8_dyadic(2, 3, 40, 128, seed=7)
+
+    def dec(c):
+        return torch.from_numpy(c).view(torch.float8_e4m3fn).double().numpy()
+
+    q, k, v = dec(q8), dec(k8), dec(v8)
+    assert set(np.unique(q)) <= {-1.0, 0.0, 1.0}
+    assert np.all((q != 0).sum(axis=-1) == 2)
+    assert set(np.unique(k)) == {-2.0, -1.0, 0.0, 1.0, 2.0}
+    assert np.all(np.isfinite(v)) and len(np.unique(v8)) > 200
+    s = np.einsum("bhid,bhjd->bhij", q, k)
+    assert np.all(s == np.round(s)) and s.min() >= -4 and s.max() <= 4
+    assert len(np.unique(s)) >= 7
+    _, _, vb = si.make_qkv_fp8_dyadic(2, 3, 40, 128, seed=7, v_binade=True)
+    vals = np.abs(dec(vb))
+    assert vals.min() >= 1.0 and vals.max() < 2.0 and len(np.unique(vb)) == 16

@@ -42,7 +42,7 @@ def _kernels(text):
 
 
 def test_all_instances_compiled(asm):
-    assert len(_kernels(asm)) == 12   # (64,64), (128,128), (192,128) x dtype x mask
+    assert len(_kernels(asm)) == 14   # 16-bit (64,64), (128,128), (192,128) x dtype x mask; FP8 128 x mask
 
 
 def test_direct_loads_have_no_sgpr_hazard(asm):
@@ -61,8 +61,8 @@ def test_no_packed_fp32(asm):
 def test_no_spills_or_scratch(asm):
     spills = [int(x) for x in re.findall(r"\.vgpr_spill_count:\s+(\d+)", asm)]
     scratch = [int(x) for x in re.findall(r"\.private_segment_fixed_size:\s+(\d+)", asm)]
-    assert len(spills) == 12 and max(spills) == 0
-    assert len(scratch) == 12 and max(scratch) == 0
+    assert len(spills) == 14 and max(spills) == 0
+    assert len(scratch) == 14 and max(scratch) == 0
 
 
 def test_checker_sees_a_planted_hazard():
