@@ -178,35 +178,49 @@ def run_grid(args, qa, torch, np):
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream(dev)
-    for name, w in si.GRID.items():
-        q, k, v = w.inputs()
-        tq, tk, tv = (torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
-                      for x in (q, k, v))
+    for name, w in list(si.GRID.items()) + list(si.GRID_FP8.items()):
+        fp8 = w.dtype == "e4m3"
+        if fp8:
+            q, k, v, scales = w.fp8_inputs()
+            tq, tk, tv = (torch.from_numpy(x).to(dev) for x in (q, k, v))
+        else:
+            q, k, v = w.inputs()
+            tq, tk, tv = (torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+                          for x in (q, k, v))
         del q, k, v
-        o = torch.empty_like(tq)
+        o = torch.empty((w.B, w.H, w.N, w.d), dtype=torch.bfloat16, device=dev)
         lse = torch.empty((w.B, w.H, w.N), dtype=torch.float32, device=dev)
+        peak = PEAK_TFLOPS_FP8 if fp8 else PEAK_TFLOPS
         per = {}
         for causal in w.causal:
-            # the C entry point directly: short launches must not wait on
+            # the C entry points directly: short launches must not wait on
             # Python-side argument checks
-            call = (tq.data_ptr(), tk.data_ptr(), tv.data_ptr(), o.data_ptr(), lse.data_ptr(),
-                    w.B, w.H, w.N, w.d, w.scale, int(causal), stream.cuda_stream, qa.QM_BF16)
+            ptrs = (tq.data_ptr(), tk.data_ptr(), tv.data_ptr(), o.data_ptr(), lse.data_ptr())
+            if fp8:
+                entry = qa.qm_attn_fwd_fp8
+                call = ptrs + (w.B, w.H, w.N, w.d) + scales + (w.scale, int(causal),
+                                                               stream.cuda_stream)
+            else:
+                entry = qa.qm_attn_fwd
+                call = ptrs + (w.B, w.H, w.N, w.d, w.scale, int(causal), stream.cuda_stream,
+                               qa.QM_BF16)
             for _ in range(args.warmup):
-                assert qa.qm_attn_fwd(*call) == qa.QM_OK
+                assert entry(*call) == qa.QM_OK
             ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
             ev[0].record(stream)
             for _ in range(args.steps):
-                qa.qm_attn_fwd(*call)
+                entry(*call)
             ev[1].record(stream)
             torch.cuda.synchronize(dev)
             ms = ev[0].elapsed_time(ev[1]) / args.steps
             tf = flops(w.B, w.H, w.N, w.d, causal) / (ms * 1e-3) / 1e12
             per["causal" if causal else "unmasked"] = {
                 "ms": round(ms, 4), "tflops": round(tf, 2),
-                "pct_of_peak": round(100.0 * tf / PEAK_TFLOPS, 2)}
+                "pct_of_peak": round(100.0 * tf / peak, 2)}
         print(json.dumps({"metric": METRIC, "grid": True, "workload": name,
                           "B": w.B, "H": w.H, "N": w.N, "d": w.d, "dtype": w.dtype,
-                          "steps": args.steps, "warmup": args.warmup, "per_launch": per}),
+                          "peak_tflops": peak, "steps": args.steps, "warmup": args.warmup,
+                          "per_launch": per}),
               flush=True)
         del tq, tk, tv, o, lse
 
@@ -225,7 +239,8 @@ def main():
     ap.add_argument("--workload", default=si.BENCH_WORKLOAD, choices=sorted(si.WORKLOADS),
                     help="named workload (default: the one the metric is quoted on)")
     ap.add_argument("--grid", action="store_true",
-                    help="measure the paper's benchmark grid instead (one JSON line per shape)")
+                    help="measure the paper's benchmark grid instead (one JSON line per shape; "
+                         "bf16 at d = 64 and 128 with both masks, then FP8 at d = 128, causal)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()

@@ -234,6 +234,13 @@ GRID = {
     for d in GRID_D for n in GRID_N
 }
 WORKLOADS.update(GRID)
+# The paper's FP8 table: the same grid at d = 128, causal mask only.
+GRID_FP8 = {
+    f"grid_fp8_d128_n{n}": Workload(f"grid_fp8_d128_n{n}", 16384 // n, 2048 // 128, n, 128,
+                                    "e4m3", (True,))
+    for n in GRID_N
+}
+WORKLOADS.update(GRID_FP8)
 
 # The workload the throughput figure is quoted on (N = 8192, d = 128).
 BENCH_WORKLOAD = "mha_b2_h32_n8192_d128_bf16"

@@ -259,3 +259,23 @@ def test_long_fp8_workload_sampled(qa, long_inputs, causal):
     Or, lr = attention_rows_fp64(q8, k8, v8, w.scale, causal, "e4m3", rows, descale=scales)
     bound = _rounding_bound(q8, k8, v8, scales, w.scale, causal, rows, O, Or)
     _gate(O, L, Or, lr, bound, f"{w.name} causal={causal} sampled rows")
+
+
+@pytest.mark.parametrize("name", sorted(si.GRID_FP8))
+def test_fp8_paper_grid_sampled(qa, name):
+    """The paper's FP8 table configuration (16k tokens per batch, hidden 2048,
+    d = 128, causal) at every sequence length, on sampled rows."""
+    import torch
+    w = si.GRID_FP8[name]
+    _say(f"case {w.name}: drawing inputs")
+    q8, k8, v8, scales = w.fp8_inputs()
+    _say(f"case {w.name}: running")
+    o, lse = qa.fwd_fp8(_codes(q8), _codes(k8), _codes(v8), scales, causal=True, scale=w.scale)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(o).all()) and bool(torch.isfinite(lse).all())
+    rows = sorted(_sample_rows(w, 24, seed=w.N))
+    ix = tuple(torch.tensor(np.array(rows).T).cuda())
+    O, L = to_host64(o[ix]), to_host64(lse[ix])
+    Or, lr = attention_rows_fp64(q8, k8, v8, w.scale, True, "e4m3", rows, descale=scales)
+    bound = _rounding_bound(q8, k8, v8, scales, w.scale, True, rows, O, Or)
+    _gate(O, L, Or, lr, bound, f"{w.name} sampled rows")
