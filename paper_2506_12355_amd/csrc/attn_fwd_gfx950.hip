@@ -144,12 +144,14 @@ struct Half<1> {  // bf16
 };
 
 // FP8 (OCP E4M3) operands: the 32x32x64 MFMA, 32 one-byte values per lane
-// (lane l: row or column l % 32, k = 32 (l / 32) + byte), unit block scales,
-// and the fp32 -> E4M3 pack of two values into one half of a word (round to
-// nearest even; the values packed here are at most 2^8, below the 448 limit).
+// (lane l: row or column l % 32, k = 32 (l / 32) + byte), and the fp32 -> E4M3
+// pack of two values into one half of a word (round to nearest even; the
+// values packed here are at most 2^8, below the 448 limit).  Zero scale
+// operands select the unscaled form of the instruction, which issues faster
+// than the block-scaled one.
 struct Fp8 {
   static __device__ __forceinline__ f32x16 mfma(i32x8 a, i32x8 b, f32x16 c) {
-    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
   }
   template <bool HIGH>   // into bits 16..31 (else 0..15) of old
   static __device__ __forceinline__ int32_t pack(float x, float y, int32_t old) {
@@ -308,6 +310,14 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
   constexpr int NMT = DV / 32;           // GEMM-II M tiles
   constexpr int GPWV = LV::NG / kWaves;  // V direct loads per wave per block
   constexpr int RING = ring_depth<DK, DV, DT>();
+  // Deferred GEMM-II: with four-block rings, GEMM-II of block j can run in
+  // block j+1's region, interleaved with that block's exponentials and GEMM-I,
+  // so that no MFMA-only stretch remains in a block.  Used where the
+  // exponentials outweigh the MFMAs (FP8, d = 64), where it gains 2-6%; at
+  // d = 128 with 16-bit inputs it gains nothing at long sequences and costs
+  // 1-3% at short ones, so GEMM-II stays at the end of its own block there.
+  constexpr bool DEFER = RING == 4 && (FP8 || DK == 64);
+  constexpr int NPB = FP8 ? 1 : 4;       // P^T operand fragments per block
 
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   char* const lds = reinterpret_cast<char*>(smem);
@@ -422,7 +432,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     // last go through the zero-size descriptor, into slots no one reads again).
     //   RING = 4: an even block loads K(j+3) and K(j+4) into K slots (Q+3) % 4
     //             and Q, an odd block V(j+1) and V(j+2) into V slots (Q+1) % 4
-    //             and (Q+2) % 4;
+    //             and (Q+2) % 4, or, when GEMM-II of block j runs during block
+    //             j+1, V(j) and V(j+1) into V slots Q and (Q+1) % 4;
     //   RING = 2: every block loads K(j+2) into K slot Q % 2 and V(j+1) into V
     //             slot (Q+1) % 2.
     auto n_dma = [](auto ph) {
@@ -437,8 +448,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
         k_load(n - second * KT::GPW, blk, (Q + 3 + second) % 4, blk < nkv ? rk : rk0);
       } else if (RING == 4) {
         const int second = n >= GPWV ? 1 : 0;
-        const int blk = j + 1 + second;
-        v_load(n - second * GPWV, blk, (Q + 1 + second) % 4, blk < nkv ? rv : rv0);
+        const int lead = DEFER ? 0 : 1;   // deferred GEMM-II reads V(j) a block later
+        const int blk = j + lead + second;
+        v_load(n - second * GPWV, blk, (Q + lead + second) % 4, blk < nkv ? rv : rv0);
       } else if (n < KT::GPW) {
         k_load(n, j + 2, Q % 2, j + 2 < nkv ? rk : rk0);
       } else {
@@ -490,8 +502,39 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
           (lds_i16x4*)(lds + vb * LV::VBYTES + v_base + g_off * LV::VGS + slot * LV::ROW + 64 * mt));
     };
 
-    // whether this wave has a visible key in block j (causal: blocks above its rows are skipped)
-    auto active = [&](int j) { return (qw < N) && (!CAUSAL || j * kBN <= qw + 31); };
+    // GEMM-II operand from V slot vb: V^T fragment t (M tile t % NMT, key step
+    // t / NMT), so consecutive MFMAs accumulate into different O tiles
+    auto v_frag = [&](int vb, int t) __attribute__((always_inline)) {
+      if constexpr (FP8) {
+        // M tile t, all 64 keys: four byte-transposing reads of 8 bytes
+        i32x8 f;
+  #pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const i32x2 x = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+              (lds_i32x2*)(lds + vb * LV::VBYTES + v8_base + 2 * c * LV::ROW + 32 * t));
+          f[2 * c] = x[0];
+          f[2 * c + 1] = x[1];
+        }
+        return f;
+      } else {
+        const int mt = t % NMT, u = t / NMT;
+        const u32x2 a0 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 0));
+        const u32x2 a1 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 1));
+        return u32x4{a0[0], a0[1], a1[0], a1[1]};
+      }
+    };
+    // GEMM-II of one block on its own: O^T += V^T P^T from V slot vb (a wave's
+    // last block, when GEMM-II is deferred)
+    auto gemm2 = [&](int vb, const Frag (&pin)[NPB]) __attribute__((always_inline)) {
+      constexpr int NV = FP8 ? NMT : 4 * NMT;
+      // one fragment in flight at a time: this runs once per wave, and reading
+      // every fragment up front would raise the register peak of the kernel
+  #pragma unroll
+      for (int t = 0; t < NV; ++t) {
+        oacc[t % NMT] = OP::mfma(v_frag(vb, t), pin[FP8 ? 0 : t / NMT], oacc[t % NMT]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
 
     // GEMM-I: two 32-key tiles of S^T for the block in K buffer kb
     auto gemm1 = [&](int kb, f32x16 (&s)[2]) {
@@ -525,20 +568,30 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     // -inf) is the block's exact maximum taken, O and l rescaled and the
     // probabilities recomputed.  Results are exact either way: O and lse use
     // the same m_run.
-    auto block = [&](auto ph, int j, int kb_next, int vb, f32x16 (&s)[2], f32x16 (&s_next)[2])
+    // vb: the V slot GEMM-II reads (block j's, or block j-1's when deferred);
+    // pin: P^T of block j-1 (deferred GEMM-II); pout: P^T of block j; first:
+    // block 0, which has no deferred GEMM-II to run
+    auto block = [&](auto ph, auto first, int j, int kb_next, int vb, f32x16 (&s)[2],
+                     f32x16 (&s_next)[2], const Frag (&pin)[NPB], Frag (&pout)[NPB])
         __attribute__((always_inline)) {
+      constexpr bool DEF = DEFER && !decltype(first)::value;   // GEMM-II of block j-1 here
       const int j0 = j * kBN;
       constexpr int AHEAD = FP8 ? 2 : 4;              // operand reads ahead of their MFMA
       constexpr int NG1 = 2 * NKS;                    // GEMM-I MFMAs per block
-      constexpr int NSLOT = NG1 > 16 ? NG1 : 16;      // slots of region 1
       constexpr int NV = FP8 ? NMT : 4 * NMT;         // GEMM-II MFMAs per block
+      constexpr int NM = DEF ? NV + NG1 : NG1;        // MFMAs of region 1
+      constexpr int NSLOT = NM > 16 ? NM : 16;        // slots of region 1
       constexpr int NDMA = n_dma(decltype(ph){});     // direct loads in this block
       constexpr int DSTRIDE = (NSLOT / 2) / NDMA > 0 ? (NSLOT / 2) / NDMA : 1;
-      // first K fragments of GEMM-I for block j+1: their LDS latency runs under
-      // the mask work below
+      // first operand fragments of region 1 (deferred: V of GEMM-II, else K of
+      // GEMM-I for block j+1): their LDS latency runs under the mask work below
       Frag kring[AHEAD];
+      Frag vring[AHEAD];
   #pragma unroll
-      for (int m = 0; m < AHEAD; ++m) kring[m] = k_read(kb_next, m % 2, m / 2);
+      for (int m = 0; m < AHEAD; ++m) {
+        if constexpr (DEF) vring[m] = v_frag(vb, m);
+        else kring[m] = k_read(kb_next, m % 2, m / 2);
+      }
 
       // mask: keys past the end of the sequence, keys after the query (causal)
       const bool need_mask = (j0 + kBN > N) || (CAUSAL && j0 + kBN - 1 > qw);
@@ -556,39 +609,19 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
       // every visible key overflows to +inf and forces the exact path below
       float mu = (m_run == -INFINITY) ? -FLT_MAX : m_run;
 
-      // GEMM-II operand: V^T fragment t (M tile t % NMT, key step t / NMT), so
-      // consecutive MFMAs accumulate into different O tiles
-      auto v_frag = [&](int t) __attribute__((always_inline)) {
-        if constexpr (FP8) {
-          // M tile t, all 64 keys: four byte-transposing reads of 8 bytes
-          i32x8 f;
-  #pragma unroll
-          for (int c = 0; c < 4; ++c) {
-            const i32x2 x = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
-                (lds_i32x2*)(lds + vb * LV::VBYTES + v8_base + 2 * c * LV::ROW + 32 * t));
-            f[2 * c] = x[0];
-            f[2 * c + 1] = x[1];
-          }
-          return f;
-        } else {
-          const int mt = t % NMT, u = t / NMT;
-          const u32x2 a0 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 0));
-          const u32x2 a1 = __builtin_bit_cast(u32x2, v_read(vb, mt, u, 1));
-          return u32x4{a0[0], a0[1], a1[0], a1[1]};
-        }
-      };
-
       // P^T operands of GEMM-II: 16-bit, four fragments of 8 values (key step
       // u = 16 keys); FP8, one fragment of all 32 of the lane's values, byte
       // j = the score of key tile j / 16, register j % 16
-      Frag pb[FP8 ? 1 : 4];
+      Frag (&pb)[NPB] = pout;
       // the pair of probabilities of chunk i (keys r0 and r0 + 1 of key tile
       // kt = i / 8, r0 = 8 ((i / 4) % 2) + 2 (i % 4)) into the operand
       auto put = [&](int i, float e0, float e1) __attribute__((always_inline)) {
         const int u = i / 4, w = i % 4;
         if constexpr (FP8) {
           const int word = 2 * u + w / 2;
-          int32_t pk = (w % 2) ? Fp8::pack<true>(e0, e1, pb[0][word]) : Fp8::pack<false>(e0, e1, 0);
+          // the low half first; the stale high half it keeps is overwritten next
+          int32_t pk = (w % 2) ? Fp8::pack<true>(e0, e1, pb[0][word])
+                               : Fp8::pack<false>(e0, e1, pb[0][word]);
           asm volatile("" : "+v"(pk));
           pb[0][word] = pk;
         } else {
@@ -623,7 +656,6 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
       // live ranges.
       s_next[0] = f32x16{};
       s_next[1] = f32x16{};
-      Frag vring[AHEAD];
       float xa[18], xb[18], ea[17], eb[17];
       float lsum_even = 0.f, lsum_odd = 0.f;
       auto arg = [&](int i, int k) __attribute__((always_inline)) {
@@ -641,13 +673,27 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
       eb[0] = __builtin_amdgcn_exp2f(xb[0]);
   #pragma unroll
       for (int sidx = 0; sidx < NSLOT; ++sidx) {
-        if ((sidx * NG1) % NSLOT == 0) {
-          const int m = sidx * NG1 / NSLOT;   // MFMA m: k-step m / 2, key tile m % 2
-          const Frag a = kring[m % AHEAD];
-          if (m + AHEAD < NG1) kring[m % AHEAD] = k_read(kb_next, (m + AHEAD) % 2, (m + AHEAD) / 2);
-          s_next[m % 2] = OP::mfma(a, qf[m / 2], s_next[m % 2]);
+        if ((sidx * NM) % NSLOT == 0) {
+          // deferred: MFMAs 0 .. NV-1 are GEMM-II of block j-1 (fragment t = m),
+          // then GEMM-I; else all are GEMM-I
+          const int m = sidx * NM / NSLOT;
+          if (DEF && m < NV) {
+            const Frag a = vring[m % AHEAD];
+            if (m + AHEAD < NV) {
+              vring[m % AHEAD] = v_frag(vb, m + AHEAD);
+            } else {
+              const int g = m + AHEAD - NV;   // first K fragments of GEMM-I
+              kring[g % AHEAD] = k_read(kb_next, g % 2, g / 2);
+            }
+            oacc[m % NMT] = OP::mfma(a, pin[FP8 ? 0 : m / NMT], oacc[m % NMT]);
+          } else {
+            const int g = DEF ? m - NV : m;   // GEMM-I MFMA g: k-step g / 2, key tile g % 2
+            const Frag a = kring[g % AHEAD];
+            if (g + AHEAD < NG1) kring[g % AHEAD] = k_read(kb_next, (g + AHEAD) % 2, (g + AHEAD) / 2);
+            s_next[g % 2] = OP::mfma(a, qf[g / 2], s_next[g % 2]);
+          }
         }
-        if (sidx >= NSLOT - AHEAD) vring[sidx - (NSLOT - AHEAD)] = v_frag(sidx - (NSLOT - AHEAD));
+        if (!DEFER && sidx >= NSLOT - AHEAD) vring[sidx - (NSLOT - AHEAD)] = v_frag(vb, sidx - (NSLOT - AHEAD));
         // this block's direct loads, spread over the first half of the region
         if (sidx % DSTRIDE == 0 && sidx / DSTRIDE < NDMA) dma(ph, sidx / DSTRIDE, j);
         const int i = slot_chunk(sidx, NSLOT);
@@ -696,18 +742,21 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
       }
       l_run += lsum;
 
-      // Straight-line region 2: GEMM-II, O^T += V^T P^T
+      // Straight-line region 2 (not deferred): GEMM-II, O^T += V^T P^T
+      if constexpr (!DEFER) {
   #pragma unroll
-      for (int t = 0; t < NV; ++t) {
-        const Frag a = vring[t % AHEAD];
-        if (t + AHEAD < NV) vring[t % AHEAD] = v_frag(t + AHEAD);
-        oacc[t % NMT] = OP::mfma(a, pb[FP8 ? 0 : t / NMT], oacc[t % NMT]);
-        __builtin_amdgcn_sched_barrier(0);
+        for (int t = 0; t < NV; ++t) {
+          const Frag a = vring[t % AHEAD];
+          if (t + AHEAD < NV) vring[t % AHEAD] = v_frag(vb, t + AHEAD);
+          oacc[t % NMT] = OP::mfma(a, pb[FP8 ? 0 : t / NMT], oacc[t % NMT]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
     };
 
     // Pipeline.  Block j (Q = j % 4) finds K(j+1) in K slot (Q+1) % RING and
-    // V(j) in V slot Q % RING, and issues direct loads (see dma above).
+    // V(j) in V slot Q % RING (RING = 4: V(j-1), for the deferred GEMM-II, in
+    // V slot (Q+3) % 4), and issues direct loads (see dma above).
     // RING = 4: one barrier per pair of blocks, after each odd block: it
     // publishes the pair's loads (each wave first waits for its own) and
     // retires the pair's reads of the slots the next pair refills, so the
@@ -716,19 +765,33 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     // (causal) come only after all the blocks it computes; it still issues
     // their loads.
     f32x16 sa[2], sb[2];
+    // P^T of the even and the odd blocks (read by the next block when deferred)
+    Frag p_even[NPB] = {}, p_odd[NPB] = {};
     auto sync = [&]() __attribute__((always_inline)) {
       __builtin_amdgcn_s_waitcnt(kWaitLoads);
       __syncthreads();
     };
-    auto iteration = [&](auto ph, int j, f32x16 (&s_cur)[2], f32x16 (&s_next)[2])
-        __attribute__((always_inline)) {
+    // Blocks this wave computes: 0 .. j_act-1 (causal: the blocks up to its
+    // last row; none for a wave past the sequence end).  It still issues the
+    // loads of the blocks after those, and takes every barrier.
+    const int j_act = (qw >= N) ? 0 : (CAUSAL ? min(nkv, (qw + 31) / kBN + 1) : nkv);
+    auto iteration = [&](auto ph, auto first, int j, f32x16 (&s_cur)[2], f32x16 (&s_next)[2],
+                         Frag (&pin)[NPB], Frag (&pout)[NPB]) __attribute__((always_inline)) {
       constexpr int Q = decltype(ph)::value;
-      if (active(j)) {
-        block(ph, j, (Q + 1) % RING, Q % RING, s_cur, s_next);
+      constexpr int VB = DEFER ? (Q + 3) % 4 : Q % RING;   // the V slot GEMM-II reads
+      if (DEFER || j < j_act) {
+        block(ph, first, j, (Q + 1) % RING, VB, s_cur, s_next, pin, pout);
       } else {
   #pragma unroll
         for (int n = 0; n < n_dma(ph); ++n) dma(ph, n, j);
       }
+      if (RING == 2 || Q % 2 == 1) sync();
+    };
+    // a block this wave skips: its loads and its barrier only
+    auto skipped = [&](auto ph, int j) __attribute__((always_inline)) {
+      constexpr int Q = decltype(ph)::value;
+  #pragma unroll
+      for (int n = 0; n < n_dma(ph); ++n) dma(ph, n, j);
       if (RING == 2 || Q % 2 == 1) sync();
     };
 
@@ -736,26 +799,64 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     load_v(0, 0);
     if (nkv > 1) load_k(1, 1);
     if (RING == 4 && nkv > 2) load_k(2, 2);
-    if (RING == 4 && nkv > 1) load_v(1, 1);
+    if (RING == 4 && !DEFER && nkv > 1) load_v(1, 1);
     __builtin_amdgcn_s_waitcnt(kWaitLoads);
     __syncthreads();
-    if (active(0)) gemm1(0, sa);
+    if (j_act > 0) gemm1(0, sa);
     __syncthreads();   // K slot 0 is refilled by block 0
 
     using C0 = std::integral_constant<int, 0>;
     using C1 = std::integral_constant<int, 1>;
     using C2 = std::integral_constant<int, 2>;
     using C3 = std::integral_constant<int, 3>;
-    for (int j = 0; j < nkv; j += 4) {
-      iteration(C0{}, j, sa, sb);
-      if (j + 1 >= nkv) break;
-      iteration(C1{}, j + 1, sb, sa);
-      if (j + 2 >= nkv) break;
-      iteration(C2{}, j + 2, sa, sb);
-      if (j + 3 >= nkv) break;
-      iteration(C3{}, j + 3, sb, sa);
+    using Later = std::false_type;
+    using First = std::true_type;
+    // Deferred: block 0 (no GEMM-II of its own to run), then the other
+    // computed blocks, the skipped ones after the last GEMM-II below.
+    // Otherwise one loop over all blocks.
+    const int j_loop = DEFER ? j_act : nkv;
+    if constexpr (DEFER) {
+      if (j_act > 0) {
+        iteration(C0{}, First{}, 0, sa, sb, p_odd, p_even);
+        for (int j = 1; j < j_act; j += 4) {
+          iteration(C1{}, Later{}, j, sb, sa, p_even, p_odd);
+          if (j + 1 >= j_act) break;
+          iteration(C2{}, Later{}, j + 1, sa, sb, p_odd, p_even);
+          if (j + 2 >= j_act) break;
+          iteration(C3{}, Later{}, j + 2, sb, sa, p_even, p_odd);
+          if (j + 3 >= j_act) break;
+          iteration(C0{}, Later{}, j + 3, sa, sb, p_odd, p_even);
+        }
+      }
+    } else {
+      for (int j = 0; j < nkv; j += 4) {
+        iteration(C0{}, Later{}, j, sa, sb, p_odd, p_even);
+        if (j + 1 >= nkv) break;
+        iteration(C1{}, Later{}, j + 1, sb, sa, p_even, p_odd);
+        if (j + 2 >= nkv) break;
+        iteration(C2{}, Later{}, j + 2, sa, sb, p_odd, p_even);
+        if (j + 3 >= nkv) break;
+        iteration(C3{}, Later{}, j + 3, sb, sa, p_even, p_odd);
+      }
     }
-    // a lone last block still ends with a barrier (kept out of the loop: a
+    // the deferred GEMM-II of the wave's last computed block, at the point
+    // where the next block would have run it (its V slot is refilled only
+    // after the next barrier)
+    if constexpr (DEFER) {
+      if (j_act > 0) {
+        if ((j_act - 1) % 2 == 0) gemm2((j_act - 1) % 4, p_even);
+        else gemm2((j_act - 1) % 4, p_odd);
+      }
+    }
+    for (int j = j_loop; j < nkv; ++j) {
+      switch (j % 4) {
+        case 0: skipped(C0{}, j); break;
+        case 1: skipped(C1{}, j); break;
+        case 2: skipped(C2{}, j); break;
+        default: skipped(C3{}, j); break;
+      }
+    }
+    // a lone last block still ends with a barrier (kept out of the loops: a
     // barrier on a loop exit path makes the register allocator spill)
     if (RING == 4 && nkv % 2 == 1) sync();
 
@@ -781,7 +882,12 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     }
   };
   run(qbs[0]);
-  if (CAUSAL && qbs[1] >= 0) run(qbs[1]);
+  if (CAUSAL && qbs[1] >= 0) {
+    // the last deferred GEMM-II reads a V slot after the final barrier, which
+    // the next block's first loads may refill
+    if (DEFER) __syncthreads();
+    run(qbs[1]);
+  }
 }
 
 template <int DK, int DV, int DT, bool CAUSAL>

@@ -58,6 +58,18 @@ def test_no_packed_fp32(asm):
         assert not bad, f"{name}: {bad[:3]}"
 
 
+def test_fp8_products_use_the_unscaled_mfma(asm):
+    """The FP8 instances pass zero block-scale operands, which the compiler maps
+    to the unscaled 32x32x64 instruction; a block-scaled form with scale code 0
+    would multiply every product by 2^-254."""
+    fp8 = {n: i for n, i in _kernels(asm).items() if "ELi2ELb" in n}   # dtype 2: FP8
+    assert len(fp8) == 2
+    for name, insts in fp8.items():
+        ops = [i.split()[0] for i in insts]
+        assert ops.count("v_mfma_f32_32x32x64_f8f6f4") >= 8, name
+        assert not any(o.startswith("v_mfma_scale") for o in ops), name
+
+
 def test_no_spills_or_scratch(asm):
     spills = [int(x) for x in re.findall(r"\.vgpr_spill_count:\s+(\d+)", asm)]
     scratch = [int(x) for x in re.findall(r"\.private_segment_fixed_size:\s+(\d+)", asm)]
