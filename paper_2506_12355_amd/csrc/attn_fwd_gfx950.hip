@@ -755,8 +755,12 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     };
 
     // Pipeline.  Block j (Q = j % 4) finds K(j+1) in K slot (Q+1) % RING and
-    // V(j) in V slot Q % RING (RING = 4: V(j-1), for the deferred GEMM-II, in
-    // V slot (Q+3) % 4), and issues direct loads (see dma above).
+    // V(j) in V slot Q % RING (deferred: V(j-1) in V slot (Q+3) % 4), and
+    // issues direct loads (see dma above).  Deferred schedule: a pair of blocks
+    // (j, j+1), j even, reads V slots (j+3) % 4 and j % 4 and loads V(j+1) and
+    // V(j+2) into slots (j+1) % 4 and (j+2) % 4, so loads and reads of one pair
+    // never share a slot; V(i) is loaded by the odd block i or i-1 and read by
+    // block i+1, after the barrier that ends that odd block.
     // RING = 4: one barrier per pair of blocks, after each odd block: it
     // publishes the pair's loads (each wave first waits for its own) and
     // retires the pair's reads of the slots the next pair refills, so the
