@@ -161,13 +161,21 @@ def cpu_baseline(w, q, k, v, max_workers=16, descale=None):
     wall = time.perf_counter() - t0
     work = len(heads) * sum(flops(1, 1, w.N, w.d, c, w.d_v) for c in w.causal)
     masks = "both masks" if len(w.causal) == 2 else ("causal" if w.causal[0] else "unmasked")
+    model = "unknown CPU"
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")),
+                         model)
+    except OSError:
+        pass
     return {
         "value": round(work / wall / 1e12, 6),
         "unit": "TFLOPS",
         "cores": cores,
         "kind": "oracle",
         "sample": (f"{len(heads)} of {w.B * w.H} (batch, head) slices of {w.name}, {masks}, "
-                   f"spread over {cores} processes with single-threaded BLAS; wall {wall:.1f} s"),
+                   f"spread over {cores} processes with single-threaded BLAS on {model}; "
+                   f"wall {wall:.1f} s"),
     }
 
 
