@@ -36,7 +36,7 @@ def _kernels(text):
     """name -> instruction list, one per kernel instance."""
     out = {}
     for m in re.finditer(r"^(_Z\w*attn_fwd_kernel\w*):\s*(?:;.*)?$", text, flags=re.M):
-        end = text.index("s_endpgm", m.end())
+        end = text.index(".Lfunc_end", m.end())   # a kernel may hold several s_endpgm
         out[m.group(1)] = instructions(text[m.end():end])
     return out
 
