@@ -279,3 +279,78 @@ def test_fp8_paper_grid_sampled(qa, name):
     Or, lr = attention_rows_fp64(q8, k8, v8, w.scale, True, "e4m3", rows, descale=scales)
     bound = _rounding_bound(q8, k8, v8, scales, w.scale, True, rows, O, Or)
     _gate(O, L, Or, lr, bound, f"{w.name} sampled rows")
+
+
+# -------------------------------------------------- memory safety, determinism
+def test_fp8_outputs_written_and_nothing_else(qa):
+    """NaN-poisoned bf16 outputs are fully overwritten (the output is two bytes
+    per element while the inputs are one); guard zones around o and lse stay
+    untouched."""
+    import torch
+    B, H, N, d = 2, 2, 197, 128
+    q8, k8, v8 = si.make_qkv_fp8_dyadic(B, H, N, d, seed=31, v_binade=True)
+    scales = (1.0, 1.0, 0.05)
+    G = 256
+    for causal in (False, True):
+        obuf = torch.full((B * H * N * d + 2 * G,), float("nan"), dtype=torch.bfloat16,
+                          device="cuda")
+        lbuf = torch.full((B * H * N + 2 * G,), float("nan"), dtype=torch.float32, device="cuda")
+        for buf in (obuf, lbuf):
+            buf[:G] = 7.0
+            buf[-G:] = 7.0
+        o = obuf[G:G + B * H * N * d].view(B, H, N, d)
+        lse = lbuf[G:G + B * H * N].view(B, H, N)
+        qa.fwd_fp8(_codes(q8), _codes(k8), _codes(v8), scales, causal=causal, scale=LN2,
+                   out=o, lse=lse)
+        torch.cuda.synchronize()
+        assert bool(torch.isfinite(o).all()) and bool(torch.isfinite(lse).all())
+        for buf in (obuf, lbuf):
+            assert bool((buf[:G] == 7.0).all()) and bool((buf[-G:] == 7.0).all())
+        Or, lr = attention_fp64(q8, k8, v8, LN2, causal, "e4m3", descale=scales)
+        PV, _ = attention_fp64(q8, k8, v8 & 0x7F, LN2, causal, "e4m3", descale=scales)
+        O, L = to_host64(o), to_host64(lse)
+        bound = np.maximum(half_ulp(Or, "bf16"), half_ulp(O, "bf16")) + _summation(N) * PV
+        _gate(O, L, Or, lr, bound, f"poisoned FP8 outputs causal={causal}")
+
+
+def test_fp8_inputs_read_only_within_bounds(qa):
+    """NaN codes right after the last head of Q, K and V never reach the
+    outputs: rows past the end of the sequence read as zeros."""
+    import torch
+    B, H, N, d = 2, 2, 197, 128
+    q8, k8, v8 = si.make_qkv_fp8_dyadic(B, H, N, d, seed=32, v_binade=True)
+    n = B * H * N * d
+    G = 2 * 64 * d
+    views = []
+    for x in (q8, k8, v8):
+        buf = torch.full((n + G,), 0x7F, dtype=torch.uint8, device="cuda")   # E4M3 NaN
+        buf[:n] = torch.from_numpy(x.reshape(-1)).cuda()
+        views.append(buf[:n].view(B, H, N, d).view(torch.float8_e4m3fn))
+    scales = (1.0, 1.0, 0.05)
+    for causal in (False, True):
+        _say(f"case guarded FP8 inputs causal={causal}")
+        o, lse = qa.fwd_fp8(*views, scales, causal=causal, scale=LN2)
+        torch.cuda.synchronize()
+        assert bool(torch.isfinite(o).all()) and bool(torch.isfinite(lse).all())
+        Or, lr = attention_fp64(q8, k8, v8, LN2, causal, "e4m3", descale=scales)
+        PV, _ = attention_fp64(q8, k8, v8 & 0x7F, LN2, causal, "e4m3", descale=scales)
+        O, L = to_host64(o), to_host64(lse)
+        bound = np.maximum(half_ulp(Or, "bf16"), half_ulp(O, "bf16")) + _summation(N) * PV
+        _gate(O, L, Or, lr, bound, f"guarded FP8 inputs causal={causal}")
+
+
+def test_fp8_bit_stable_across_runs_and_streams(qa):
+    import torch
+    w = si.WORKLOADS["fp8_b2_h3_n333_d128"]
+    q8, k8, v8, scales = w.fp8_inputs()
+    tq, tk, tv = _codes(q8), _codes(k8), _codes(v8)
+    for causal in (False, True):
+        ref_o, ref_l = qa.fwd_fp8(tq, tk, tv, scales, causal=causal)
+        torch.cuda.synchronize()
+        s = torch.cuda.Stream()
+        for rep in range(3):
+            with torch.cuda.stream(s if rep == 2 else torch.cuda.current_stream()):
+                o, l = qa.fwd_fp8(tq, tk, tv, scales, causal=causal)
+            torch.cuda.synchronize()
+            assert torch.equal(o.view(torch.int16), ref_o.view(torch.int16))
+            assert torch.equal(l.view(torch.int32), ref_l.view(torch.int32))

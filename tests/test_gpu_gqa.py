@@ -132,3 +132,23 @@ def test_gqa_entry_with_all_heads_is_mha(qa):
         torch.cuda.synchronize()
         assert torch.equal(outs[0][0].view(torch.int16), outs[1][0].view(torch.int16))
         assert torch.equal(outs[0][1].view(torch.int32), outs[1][1].view(torch.int32))
+
+
+def test_gqa_inputs_read_only_within_bounds(qa):
+    """NaN right after the last key/value head (Hkv of them) and the last query
+    head never reaches the outputs."""
+    import torch
+    B, H, Hkv, N, d = 2, 4, 2, 197, 128
+    q, k, v = si.make_qkv(B, H, N, d, "bf16", seed=43, Hkv=Hkv)
+    views = []
+    for x in (q, k, v):
+        t = to_device(x, "bf16").reshape(-1)
+        buf = torch.full((t.numel() + 2 * 64 * d,), float("nan"), dtype=t.dtype, device="cuda")
+        buf[:t.numel()] = t
+        views.append(buf[:t.numel()].view(x.shape))
+    for causal in (False, True):
+        o, lse = qa.fwd(*views, causal=causal)
+        torch.cuda.synchronize()
+        assert bool(torch.isfinite(o).all()) and bool(torch.isfinite(lse).all())
+        Or, lr = attention_fp64(q, k, v, si.default_scale(d), causal, "bf16")
+        check_close(to_host64(o), to_host64(lse), Or, lr, "bf16", f"guarded GQA causal={causal}")

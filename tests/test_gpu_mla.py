@@ -114,3 +114,45 @@ def test_zero_rope_part_equals_mha(qa, N, dtype):
                       v, dtype, causal, scale)
         assert torch.equal(o.view(torch.int16), o2.view(torch.int16))
         assert torch.equal(lse.view(torch.int32), l2.view(torch.int32))
+
+
+def test_mla_inputs_read_only_within_bounds(qa):
+    """NaN right after the last head of Q, K (192 wide) and V (128 wide) never
+    reaches the outputs; NaN-poisoned outputs are fully overwritten and their
+    guard zones untouched."""
+    import torch
+    B, H, N = 2, 2, 197
+    q, k, v = si.make_qkv(B, H, N, 192, "bf16", seed=41, dv=128)
+    views = []
+    for x in (q, k, v):
+        t = to_device(x, "bf16").reshape(-1)
+        buf = torch.full((t.numel() + 2 * 64 * 192,), float("nan"), dtype=t.dtype, device="cuda")
+        buf[:t.numel()] = t
+        views.append(buf[:t.numel()].view(x.shape))
+    G = 256
+    for causal in (False, True):
+        _say(f"case guarded MLA inputs causal={causal}")
+        obuf = torch.full((B * H * N * 128 + 2 * G,), float("nan"), dtype=torch.bfloat16,
+                          device="cuda")
+        obuf[:G] = 7.0
+        obuf[-G:] = 7.0
+        o = obuf[G:G + B * H * N * 128].view(B, H, N, 128)
+        o, lse = qa.fwd(*views, causal=causal, scale=si.default_scale(192), out=o)
+        torch.cuda.synchronize()
+        assert bool(torch.isfinite(o).all()) and bool(torch.isfinite(lse).all())
+        assert bool((obuf[:G] == 7.0).all()) and bool((obuf[-G:] == 7.0).all())
+        Or, lr = attention_fp64(q, k, v, si.default_scale(192), causal, "bf16")
+        check_close(to_host64(o), to_host64(lse), Or, lr, "bf16", f"guarded MLA causal={causal}")
+
+
+def test_mla_bit_stable_across_runs(qa):
+    import torch
+    q, k, v = si.make_qkv(2, 3, 555, 192, "f16", seed=42, dv=128)
+    tq, tk, tv = (to_device(x, "f16") for x in (q, k, v))
+    for causal in (False, True):
+        ref_o, ref_l = qa.fwd(tq, tk, tv, causal=causal)
+        for _ in range(2):
+            o, l = qa.fwd(tq, tk, tv, causal=causal)
+            torch.cuda.synchronize()
+            assert torch.equal(o.view(torch.int16), ref_o.view(torch.int16))
+            assert torch.equal(l.view(torch.int32), ref_l.view(torch.int32))
