@@ -354,3 +354,19 @@ def test_fp8_bit_stable_across_runs_and_streams(qa):
             torch.cuda.synchronize()
             assert torch.equal(o.view(torch.int16), ref_o.view(torch.int16))
             assert torch.equal(l.view(torch.int32), ref_l.view(torch.int32))
+
+
+@pytest.mark.parametrize("N", [1, 65, 1000])
+def test_fp8_general_inputs_edge_lengths(qa, N):
+    """General FP8 inputs (normal draws scaled to the E4M3 range) at ragged
+    lengths, compared in full under the rounding bound."""
+    q8, k8, v8, scales = si.make_qkv_fp8(2, 3, N, 128, seed=50 + N)
+    scale = si.default_scale(128)
+    rows = [(b, h, i) for b in range(2) for h in range(3) for i in range(N)]
+    for causal in (False, True):
+        _say(f"case FP8 general inputs N={N} causal={causal}")
+        O, lse = _run(qa, q8, k8, v8, scales, causal, scale)
+        Or, lr = attention_fp64(q8, k8, v8, scale, causal, "e4m3", descale=scales)
+        Of, Orf = O.reshape(-1, 128), Or.reshape(-1, 128)
+        bound = _rounding_bound(q8, k8, v8, scales, scale, causal, rows, Of, Orf)
+        _gate(Of, lse.ravel(), Orf, lr.ravel(), bound, f"FP8 general N={N} causal={causal}")
