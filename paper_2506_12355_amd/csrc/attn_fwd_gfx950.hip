@@ -9,7 +9,8 @@
 // sequence in blocks of BN = 64 keys (the loop of the paper's Appendix B
 // listings).  A K/V block staged in LDS serves all 256 rows.
 //
-// The two products use the 32x32x16 MFMA of CDNA4:
+// The two products use the 32x32x16 MFMA of CDNA4 (FP8 inputs: the 32x32x64
+// one, with ds_read_b64_tr_b8 for V^T and E4M3 packs for P^T; see Fp8 below):
 //
 //   GEMM-I   S^T[key][query] = K[key][:] . Q[query][:]
 //            A operand = K rows read from LDS (K keeps its stored layout, the
@@ -32,11 +33,13 @@
 //
 // Pipeline: K and V blocks go HBM -> LDS with direct buffer loads
 // (buffer_load_dwordx4 ... lds; rows past the end of the sequence read as
-// zeros) into four-block rings, K one block further ahead than V, each wave's
-// loads spread over its MFMA slots.  While the exponentials of block j are
-// formed, the MFMAs of GEMM-I for block j+1 run beside them (16 interleaved
-// slots, the exponentials software-pipelined three deep, the wave at raised
-// issue priority); then GEMM-II of block j.  One barrier per two blocks.
+// zeros) into four-block rings (two-block rings for 192-wide keys), K further
+// ahead than V, each wave's loads spread over its MFMA slots.  While the
+// exponentials of block j are formed, the MFMAs of GEMM-I for block j+1 run
+// beside them (16 interleaved slots, the exponentials software-pipelined three
+// deep, the wave at raised issue priority); then GEMM-II of block j, or, for
+// FP8 and d = 64, GEMM-II of block j-1 in the same interleaved region (see
+// DEFER below).  One barrier per two blocks (per block with two-block rings).
 //
 // Online softmax (exp2 domain, c = |scale| * log2 e): probabilities
 // p = 2^(c s - m) are formed against the running maximum m without first
@@ -50,11 +53,16 @@
 // Causal masking: key blocks entirely above the diagonal of the workgroup are
 // never loaded; a wavefront skips the blocks entirely above its own rows;
 // elementwise masking runs only on blocks that straddle the diagonal or the
-// sequence tail.  Heavy (late) query blocks are dispatched first.
+// sequence tail.  A workgroup runs a long and a short query block, the long
+// one first, so that all workgroups cost the same.
 //
 // Dispatch order: workgroup i runs on XCD i % 8.  The linear id is remapped so
-// that consecutive query blocks of the same head land on the same XCD and
-// share its L2 for the K/V stream.
+// that consecutive query blocks of the same head (and the heads sharing one
+// key/value head) land on the same XCD and share its L2 for the K/V stream.
+//
+// Shapes: head dimension 64 or 128 (q, k, v alike), or 192-wide queries and
+// keys with 128-wide values (the MLA shape); H query heads may share Hkv
+// key/value heads (grouped-query and multi-query attention).
 
 #include <hip/hip_runtime.h>
 #include <float.h>
