@@ -98,7 +98,7 @@ constexpr int kBN = 64;       // keys per block
 constexpr int kWaves = 8;     // 32 query rows per wavefront
 constexpr int kThreads = 64 * kWaves;
 // Largest probability allowed against a stale running maximum, 2^8: sums of
-// 64K such values stay far from fp32 overflow and P fits fp16.
+// 64K such values stay far from fp32 overflow, and P fits fp16 and E4M3 (448).
 constexpr float kPmax = 256.0f;
 constexpr int kXcds = 8;
 constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data
@@ -557,7 +557,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
 
     // Block j: mask, row max and (rare) rescale; then, in one straight-line
     // region, the exponentials of block j interleaved with the MFMAs of GEMM-I
-    // for block j+1; then GEMM-II of block j.  GEMM-I always runs: on a wave's
+    // for block j+1 (and, deferred, of GEMM-II for block j-1); then GEMM-II of
+    // block j unless deferred.  GEMM-I always runs: on a wave's
     // last block it reads a stale (in-bounds) K buffer and its result is dropped,
     // which keeps a single code path and the register allocation compact.
     // row maximum of a block's (masked) scores, both lane halves, raw units
@@ -570,7 +571,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
 
     // Block j.  Probabilities are formed against the running maximum m_run
     // without looking at the block's own maximum; since every p >= 0, a lane
-    // whose 32 probabilities sum to at most 2^TAU has every p <= 2^TAU, which
+    // whose 32 probabilities sum to at most 2^8 (kPmax) has every p <= 2^8, which
     // keeps all sums in range.  Only when some lane exceeds that (the running
     // maximum must rise, and always on a wave's first block, where m_run is
     // -inf) is the block's exact maximum taken, O and l rescaled and the
@@ -652,16 +653,17 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
         lsum += e0 + e1;
       };
 
-      // Straight-line region 1, written as NSLOT slots (16, or 24 when GEMM-I
-      // has 24 MFMAs at DK = 192).  The slots issue the MFMAs of GEMM-I for
-      // block j+1 (every slot at DK = 128 and 192, every other slot at 64) and
-      // advance the 16 exponential chunks of block j through a three-stage
-      // software pipeline: the FMAs of pair i+2, the exponentials of pair i+1,
-      // and the pack and row-sum adds of pair i, so that no instruction waits
-      // on a result produced in its own slot.  Operand reads run AHEAD MFMAs
-      // early from small register rings (the last slots start on GEMM-II's V
-      // fragments); a scheduling fence after each slot keeps the order and the
-      // live ranges.
+      // Straight-line region 1, written as NSLOT = max(NM, 16) slots for its NM
+      // MFMAs: GEMM-I for block j+1 (16 at DK = 128, 24 at DK = 192, 8 at 64,
+      // 4 for FP8), preceded, when GEMM-II is deferred, by GEMM-II of block j-1
+      // (8 at d = 64, 4 for FP8).  The MFMAs are spread evenly over the slots,
+      // and the slots advance the 16 exponential chunks of block j through a
+      // three-stage software pipeline: the FMAs of pair i+2, the exponentials
+      // of pair i+1, and the pack and row-sum adds of pair i, so that no
+      // instruction waits on a result produced in its own slot.  Operand reads
+      // run AHEAD MFMAs early from small register rings (the last slots start
+      // on the next MFMA kind's fragments); a scheduling fence after each slot
+      // keeps the order and the live ranges.
       s_next[0] = f32x16{};
       s_next[1] = f32x16{};
       float xa[18], xb[18], ea[17], eb[17];
