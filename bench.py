@@ -246,6 +246,9 @@ def main():
                          "under a profiler that initialises the GPU in every process")
     ap.add_argument("--workload", default=si.BENCH_WORKLOAD, choices=sorted(si.WORKLOADS),
                     help="named workload (default: the one the metric is quoted on)")
+    ap.add_argument("--layout", default="bhnd", choices=("bhnd", "bnhd"),
+                    help="memory layout of q, k, v and o for 16-bit workloads: [B][H][N][d] "
+                         "(default) or [B][N][H][d]")
     ap.add_argument("--grid", action="store_true",
                     help="measure the paper's benchmark grid instead (one JSON line per shape; "
                          "bf16 at d = 64 and 128 with both masks, then FP8 at d = 128, causal)")
@@ -287,10 +290,16 @@ def main():
         scales = None
         tdtype = torch.bfloat16 if w.dtype == "bf16" else torch.float16
         tq, tk, tv = (torch.from_numpy(x.view(np.int16)).to(dev).view(tdtype) for x in (q, k, v))
+        if args.layout == "bnhd":
+            tq, tk, tv = (t.transpose(1, 2).contiguous() for t in (tq, tk, tv))
+    if fp8 and args.layout != "bhnd":
+        print("the FP8 entry point takes [B][H][N][d] only", file=sys.stderr)
+        sys.exit(2)
     peak = PEAK_TFLOPS_FP8 if fp8 else PEAK_TFLOPS
     peak_per_clk = PEAK_FLOP_PER_CLK_FP8 if fp8 else PEAK_FLOP_PER_CLK
     masks = list(w.causal)
-    outs = [(torch.empty((w.B, w.H, w.N, w.d_v), dtype=tdtype, device=dev),
+    oshape = (w.B, w.N, w.H, w.d_v) if args.layout == "bnhd" else (w.B, w.H, w.N, w.d_v)
+    outs = [(torch.empty(oshape, dtype=tdtype, device=dev),
              torch.empty((w.B, w.H, w.N), dtype=torch.float32, device=dev))
             for _ in masks]
     stream = torch.cuda.current_stream(dev)
@@ -304,7 +313,7 @@ def main():
                            lse=outs[m][1], stream=stream)
             else:
                 qa.fwd(tq, tk, tv, causal=causal, scale=w.scale, out=outs[m][0],
-                       lse=outs[m][1], stream=stream)
+                       lse=outs[m][1], stream=stream, layout=args.layout)
         if ev is not None:
             ev[len(masks)].record(stream)
 
@@ -354,6 +363,7 @@ def main():
             "workload": f"{w.name}: {' + '.join(mask_name)} forward per step",
             "B": w.B, "H": w.H, "Hkv": w.kv_heads, "N": w.N, "d": w.d, "d_v": w.d_v,
             "dtype": w.dtype,
+            "layout": "[B][N][H][d]" if args.layout == "bnhd" else "[B][H][N][d]",
             "flop_count": ("4·B·H·N²·d" if w.d_v == w.d else "2·B·H·N²·(d + d_v)") + ", ½ if causal",
             "masks": ["causal" if c else "none" for c in masks], "seed": w.seed,
         },
@@ -372,7 +382,8 @@ def main():
             "peak": peak,
             "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4),
-            "traffic": committed_traffic() if w.name == si.BENCH_WORKLOAD else None,
+            "traffic": (committed_traffic()
+                        if w.name == si.BENCH_WORKLOAD and args.layout == "bhnd" else None),
         },
     }
     if not args.no_cpu_baseline:

@@ -43,12 +43,19 @@ typedef enum {
   QM_BF16 = 1  /* bfloat16 (top half of an IEEE binary32) */
 } qm_dtype_t;
 
+/* Memory layouts of q, k, v and o (qm_attn_fwd_layout; lse is always [B][H][N]). */
+typedef enum {
+  QM_BHND = 0,  /* [B][heads][N][width]: each head a contiguous N x width slab */
+  QM_BNHD = 1   /* [B][N][heads][width]: each token's heads side by side */
+} qm_layout_t;
+
 /* Status codes returned by every qm_attn_fwd* entry point. */
 enum {
   QM_OK = 0,
   QM_ERR_NULL = -1,        /* q, k, v, o or lse is NULL */
-  QM_ERR_SHAPE = -2,       /* B, H or N < 1, Hkv not a divisor of H, or B*H*N*d
-                              does not fit in 62 bits */
+  QM_ERR_SHAPE = -2,       /* B, H or N < 1, Hkv not a divisor of H, B*H*N*d
+                              does not fit in 62 bits, or (N + 256) * d (QM_BNHD:
+                              times the heads, in bytes) does not fit in 31 (32) bits */
   QM_ERR_HEADDIM = -3,     /* d is not 64 or 128 (qm_attn_fwd_mla: (d_qk, d_v) is not
                               (64, 64), (128, 128) or (192, 128)) */
   QM_ERR_DTYPE = -4,       /* dtype is not QM_F16 or QM_BF16 */
@@ -57,7 +64,9 @@ enum {
   QM_ERR_ALIAS = -6,       /* o or lse overlaps q, k, v or each other */
   QM_ERR_CAUSAL = -7,      /* causal is neither 0 nor 1 */
   QM_ERR_LAUNCH = -8,      /* the HIP runtime rejected the kernel launch */
-  QM_ERR_UNSUPPORTED = -9  /* a pointer is not 16-byte aligned */
+  QM_ERR_UNSUPPORTED = -9, /* a pointer is not 16-byte aligned */
+  QM_ERR_LAYOUT = -10      /* layout is not QM_BHND or QM_BNHD, or QM_BNHD with
+                              d_qk = 192 */
 };
 
 /*
@@ -161,6 +170,29 @@ int qm_attn_fwd_mla(const void* q, const void* k, const void* v, void* o, float*
 int qm_attn_fwd_fp8(const void* q, const void* k, const void* v, void* o, float* lse,
                     int B, int H, int N, int d, float q_scale, float k_scale, float v_scale,
                     float scale, int causal, hipStream_t stream);
+
+/*
+ * qm_attn_fwd_layout - the 16-bit entry points in one call, with the memory
+ * layout as an argument.  Computes exactly what qm_attn_fwd_gqa (Hkv < H) and
+ * qm_attn_fwd_mla (d_qk = 192, d_v = 128) compute, on tensors stored as
+ * `layout`:
+ *
+ *   QM_BHND  q [B][H][N][d_qk], k [B][Hkv][N][d_qk], v [B][Hkv][N][d_v],
+ *            o [B][H][N][d_v] (the other entry points' layout);
+ *   QM_BNHD  q [B][N][H][d_qk], k [B][N][Hkv][d_qk], v [B][N][Hkv][d_v],
+ *            o [B][N][H][d_v]: the layout a projection writes before any
+ *            transpose.
+ *
+ *   lse      [out] device, [B][H][N] float32 in either layout.
+ *   (d_qk, d_v)    (64, 64), (128, 128) or (192, 128); QM_ERR_HEADDIM otherwise.
+ *   layout         a qm_layout_t; QM_BNHD takes (d_qk, d_v) = (64, 64) or
+ *                  (128, 128).  QM_ERR_LAYOUT otherwise.
+ *   all other arguments, the arithmetic, determinism and the status codes are
+ *   those of qm_attn_fwd.  Both layouts give byte-identical results.
+ */
+int qm_attn_fwd_layout(const void* q, const void* k, const void* v, void* o, float* lse,
+                       int B, int H, int Hkv, int N, int d_qk, int d_v, float scale,
+                       int causal, hipStream_t stream, int dtype, int layout);
 
 /* qm_attn_strerror - a static, human-readable string for a status code. */
 const char* qm_attn_strerror(int status);

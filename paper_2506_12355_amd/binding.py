@@ -17,6 +17,10 @@ LIB_PATH = os.path.join(PKG_DIR, "libqm_attn.so")
 QM_F16 = 0
 QM_BF16 = 1
 
+# qm_layout_t
+QM_BHND = 0
+QM_BNHD = 1
+
 # status codes
 QM_OK = 0
 QM_ERR_NULL = -1
@@ -28,6 +32,7 @@ QM_ERR_ALIAS = -6
 QM_ERR_CAUSAL = -7
 QM_ERR_LAUNCH = -8
 QM_ERR_UNSUPPORTED = -9
+QM_ERR_LAYOUT = -10
 
 _lib = None
 _lock = threading.Lock()
@@ -77,6 +82,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
             ctypes.c_void_p,
         ]
         lib.qm_attn_fwd_fp8.restype = ctypes.c_int
+        lib.qm_attn_fwd_layout.argtypes = [
+            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+            ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+            ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+        ]
+        lib.qm_attn_fwd_layout.restype = ctypes.c_int
         lib.qm_attn_strerror.argtypes = [ctypes.c_int]
         lib.qm_attn_strerror.restype = ctypes.c_char_p
         _lib = lib
@@ -91,6 +102,15 @@ def qm_attn_fwd(q, k, v, o, lse, B, H, N, d, scale, causal, stream, dtype) -> in
     """The C entry point with plain integers for pointers; returns the status."""
     return load_library().qm_attn_fwd(q, k, v, o, lse, int(B), int(H), int(N), int(d),
                                       float(scale), int(causal), stream, int(dtype))
+
+
+def qm_attn_fwd_layout(q, k, v, o, lse, B, H, Hkv, N, d_qk, d_v, scale, causal, stream, dtype,
+                       layout) -> int:
+    """The general 16-bit C entry point (layout argument) with plain integers
+    for pointers; returns the status."""
+    return load_library().qm_attn_fwd_layout(q, k, v, o, lse, int(B), int(H), int(Hkv), int(N),
+                                             int(d_qk), int(d_v), float(scale), int(causal),
+                                             stream, int(dtype), int(layout))
 
 
 def qm_attn_fwd_gqa(q, k, v, o, lse, B, H, Hkv, N, d, scale, causal, stream, dtype) -> int:
@@ -162,24 +182,35 @@ def _dtype_code(t) -> int:
 
 
 def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse=None,
-        stream=None):
+        stream=None, layout: str = "bhnd"):
     """Attention forward on torch tensors on a ROCm device.
 
     q is [B, H, N, d]; k is [B, Hkv, N, d] and v [B, Hkv, N, dv] with Hkv
     dividing H.  Hkv = H and dv = d: multi-head attention (``qm_attn_fwd``);
     Hkv < H: grouped-query or multi-query attention (``qm_attn_fwd_gqa``);
     dv < d (d = 192, dv = 128, Hkv = H): the MLA shape (``qm_attn_fwd_mla``).
-    Returns (o, lse): o is [B, H, N, dv] of q's dtype, lse is float32
-    [B, H, N].  ``scale`` defaults to 1/sqrt(d) rounded to float32.
-    ``stream`` defaults to the current stream of q's device.
+    With ``layout="bnhd"`` the tensors are [B, N, heads, width] instead (q
+    [B, N, H, d], k [B, N, Hkv, d], v [B, N, Hkv, dv], o [B, N, H, dv];
+    ``qm_attn_fwd_layout``).  Returns (o, lse): o of q's dtype, lse float32
+    [B, H, N] in either layout.  ``scale`` defaults to 1/sqrt(d) rounded to
+    float32.  ``stream`` defaults to the current stream of q's device.
     """
     import torch
 
+    if layout not in ("bhnd", "bnhd"):
+        raise ValueError(f"layout must be 'bhnd' or 'bnhd', not {layout!r}")
+    bnhd = layout == "bnhd"
+    names = "[B, N, H, d]" if bnhd else "[B, H, N, d]"
     if q.dim() != 4:
-        raise ValueError("q must have shape [B, H, N, d]")
-    if k.dim() != 4 or v.dim() != 4 or v.shape[:3] != k.shape[:3]:
-        raise ValueError("k must be [B, Hkv, N, d] and v [B, Hkv, N, dv]")
-    if k.shape[0] != q.shape[0] or k.shape[2:] != q.shape[2:]:
+        raise ValueError(f"q must have shape {names}")
+
+    def shape(t):   # (B, heads, N, width) whatever the layout
+        s = tuple(t.shape)
+        return (s[0], s[2], s[1], s[3]) if bnhd else s
+
+    if k.dim() != 4 or v.dim() != 4 or shape(v)[:3] != shape(k)[:3]:
+        raise ValueError("k must hold Hkv heads of width d and v Hkv heads of width dv")
+    if shape(k)[0] != shape(q)[0] or shape(k)[2:] != shape(q)[2:]:
         raise ValueError("k must match q in B, N and d")
     if not (q.is_cuda and k.is_cuda and v.is_cuda):
         raise ValueError("q, k and v must be on a ROCm device")
@@ -188,25 +219,31 @@ def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse
     if not (q.dtype == k.dtype == v.dtype):
         raise TypeError("q, k and v must have the same dtype")
     if not (q.is_contiguous() and k.is_contiguous() and v.is_contiguous()):
-        raise ValueError("q, k and v must be contiguous [B, H, N, d]")
-    B, H, N, d = q.shape
-    dv = v.shape[3]
+        raise ValueError(f"q, k and v must be contiguous {names}")
+    B, H, N, d = shape(q)
+    dv = shape(v)[3]
+    Hkv = shape(k)[1]
     code = _dtype_code(q)
     if scale is None:
         scale = float(torch.tensor(1.0 / d ** 0.5, dtype=torch.float32))
+    oshape = (B, N, H, dv) if bnhd else (B, H, N, dv)
     if out is None:
-        out = torch.empty((B, H, N, dv), dtype=q.dtype, device=q.device)
-    elif out.shape != (B, H, N, dv) or out.dtype != q.dtype or not out.is_contiguous():
-        raise ValueError("out must be a contiguous [B, H, N, dv] tensor of q's dtype")
+        out = torch.empty(oshape, dtype=q.dtype, device=q.device)
+    elif tuple(out.shape) != oshape or out.dtype != q.dtype or not out.is_contiguous():
+        raise ValueError(f"out must be a contiguous {list(oshape)} tensor of q's dtype")
     if lse is None:
         lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
     elif lse.shape != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous():
         raise ValueError("lse must be a contiguous float32 tensor of shape [B, H, N]")
     if stream is None:
         stream = torch.cuda.current_stream(q.device)
-    Hkv = k.shape[1]
     with torch.cuda.device(q.device):
-        if dv != d:
+        if bnhd:
+            status = qm_attn_fwd_layout(q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                                        out.data_ptr(), lse.data_ptr(), B, H, Hkv, N, d, dv,
+                                        scale, 1 if causal else 0, stream.cuda_stream, code,
+                                        QM_BNHD)
+        elif dv != d:
             if Hkv != H:
                 raise ValueError("unequal head dimensions need as many key/value heads as query heads")
             status = qm_attn_fwd_mla(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),

@@ -122,6 +122,7 @@ struct KParams {
   float c;     // |scale| * log2 e (FP8: |scale * q_scale * k_scale| * log2 e)
   float vscale;  // factor of O: 1, or the FP8 value scale
   int qmode;
+  int layout;    // 0: q, k, v, o as [B][heads][N][width]; 1: as [B][N][heads][width]
 };
 
 // 16-bit type traits: the MFMA and the fp32 -> 16-bit pack (round to nearest
@@ -357,11 +358,27 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
   // workgroups run on one XCD and share its L2 for the K/V stream.
   const int b = bh / p.H;
   const int bhkv = b * p.Hkv + (bh - b * p.H) / p.group;
-  const uint32_t head_bytes_k = (uint32_t)N * DK * ES;  // one head of q or k
-  const uint32_t head_bytes_v = (uint32_t)N * DV * ES;  // one head of v
-  const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + (size_t)bh * N * DK * ES, head_bytes_k);
-  const i32x4 rk = make_dma_rsrc(p.k + (size_t)bhkv * N * DK * ES, head_bytes_k);
-  const i32x4 rv = make_dma_rsrc(p.v + (size_t)bhkv * N * DV * ES, head_bytes_v);
+  // One head's rows: w bytes each, rs bytes apart ([B][heads][N][w]: rs = w,
+  // heads contiguous; [B][N][heads][w]: rs = heads * w, heads interleaved).
+  // Every access goes through a buffer resource spanning exactly the head's
+  // rows, (N - 1) rs + w bytes, so rows past the end read as zeros and
+  // stores to them are dropped.
+  // (The two-block-ring instances, 192-wide keys, take [B][heads][N][w] only:
+  // runtime strides there spill registers.)
+  const bool bnhd = RING == 4 && p.layout != 0;
+  constexpr uint32_t WQ = DK * ES, WV = DV * ES, WO = DV * 2;
+  const uint32_t rs_q = bnhd ? p.H * WQ : WQ;
+  const uint32_t rs_k = bnhd ? p.Hkv * WQ : WQ;
+  const uint32_t rs_v = bnhd ? p.Hkv * WV : WV;
+  const uint32_t rs_o = bnhd ? p.H * WO : WO;
+  auto head_off = [&](int bb, int h, int heads, uint32_t w) -> size_t {
+    return bnhd ? ((size_t)bb * N * heads + h) * w : ((size_t)bb * heads + h) * N * w;
+  };
+  auto span = [&](uint32_t rs, uint32_t w) { return (uint32_t)(N - 1) * rs + w; };
+  const int h_q = bh - b * p.H, h_kv = bhkv - b * p.Hkv;
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + head_off(b, h_q, p.H, WQ), span(rs_q, WQ));
+  const i32x4 rk = make_dma_rsrc(p.k + head_off(b, h_kv, p.Hkv, WQ), span(rs_k, WQ));
+  const i32x4 rv = make_dma_rsrc(p.v + head_off(b, h_kv, p.Hkv, WV), span(rs_v, WV));
   // zero-size descriptors: a load through one touches no memory and writes zeros
   const i32x4 rk0 = i32x4{rk[0], rk[1], 0, rk[3]};
   const i32x4 rv0 = i32x4{rv[0], rv[1], 0, rv[3]};
@@ -376,7 +393,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     Frag qf[NKS];
   #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
-      const uint32_t off = (uint32_t)(qrow * DK * ES + ks * OP::KSTEP * ES + hi * OP::KGB);
+      const uint32_t off = (uint32_t)qrow * rs_q + (uint32_t)(ks * OP::KSTEP * ES + hi * OP::KGB);
       if constexpr (FP8) {
         const u32x4 lo = __builtin_amdgcn_raw_buffer_load_b128(rq, off, 0, 0);
         const u32x4 up = __builtin_amdgcn_raw_buffer_load_b128(rq, off + 16, 0, 0);
@@ -404,28 +421,29 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     constexpr int VOFF = RING * KT::BYTES;
     // lane parts of the global offsets (row slot, 16-byte unit, column of the
     // K part); the row of the load group is added per load
-    const uint32_t koff0 = (uint32_t)(KT::L0::NG * (lane / KT::L0::U) * DK * ES + (lane % KT::L0::U) * 16);
-    const uint32_t koff1 = (uint32_t)(KT::L1::NG * (lane / KT::L1::U) * DK * ES + KT::W0 * ES +
-                                      (lane % KT::L1::U) * 16);
-    const uint32_t voff = (uint32_t)(LV::NG * (lane / LV::U) * DV * ES + (lane % LV::U) * 16);
+    const uint32_t koff0 = (uint32_t)(KT::L0::NG * (lane / KT::L0::U)) * rs_k +
+                           (uint32_t)((lane % KT::L0::U) * 16);
+    const uint32_t koff1 = (uint32_t)(KT::L1::NG * (lane / KT::L1::U)) * rs_k +
+                           (uint32_t)(KT::W0 * ES + (lane % KT::L1::U) * 16);
+    const uint32_t voff = (uint32_t)(LV::NG * (lane / LV::U)) * rs_v + (uint32_t)((lane % LV::U) * 16);
     auto lds_addr = [&](int byte_off) { return (uint32_t)(uintptr_t)(lds_void*)(lds + byte_off); };
     // load i (of KT::GPW) of this wave for K block blk into K slot kb
     auto k_load = [&](int i, int blk, int kb, i32x4 rs) __attribute__((always_inline)) {
       if (i < KT::GPW0) {
         const int g = wave * KT::GPW0 + i;
         lds_load16(rs, lds_addr(kb * KT::BYTES + g * KT::L0::KGS),
-                   koff0 + (uint32_t)((blk * kBN + g) * DK) * ES);
+                   koff0 + (uint32_t)(blk * kBN + g) * rs_k);
       } else {
         const int g = wave * KT::GPW1 + (i - KT::GPW0);
         lds_load16(rs, lds_addr(kb * KT::BYTES + KT::OFF1 + g * KT::L1::KGS),
-                   koff1 + (uint32_t)((blk * kBN + g) * DK) * ES);
+                   koff1 + (uint32_t)(blk * kBN + g) * rs_k);
       }
     };
     // load i (of GPWV) of this wave for V block blk into V slot vb
     auto v_load = [&](int i, int blk, int vb, i32x4 rs) __attribute__((always_inline)) {
       const int g = wave * GPWV + i;
       lds_load16(rs, lds_addr(VOFF + vb * LV::VBYTES + g * LV::VGS),
-                 voff + (uint32_t)((blk * kBN + g) * DV) * ES);
+                 voff + (uint32_t)(blk * kBN + g) * rs_v);
     };
     auto load_k = [&](int blk, int kb) {
   #pragma unroll
@@ -878,7 +896,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
     const float l_tot = sum_across_halves(l_run);
     const float inv = p.vscale / l_tot;
     // the output is 16-bit for every input type (FP8 inputs give bf16)
-    const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.o + (size_t)bh * N * DV, (uint32_t)N * DV * 2);
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.o + head_off(b, h_q, p.H, WO) / 2, span(rs_o, WO));
   #pragma unroll
     for (int mt = 0; mt < NMT; ++mt) {
   #pragma unroll
@@ -886,7 +904,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
         using OutT = Half<FP8 ? 1 : DT>;   // FP8 inputs give a bf16 output
         const u32x2 w = {OutT::pack(oacc[mt][4 * g] * inv, oacc[mt][4 * g + 1] * inv),
                          OutT::pack(oacc[mt][4 * g + 2] * inv, oacc[mt][4 * g + 3] * inv)};
-        __builtin_amdgcn_raw_buffer_store_b64(w, ro, (uint32_t)(qrow * DV + 32 * mt + 8 * g + 4 * hi) * 2, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b64(
+            w, ro, (uint32_t)qrow * rs_o + (uint32_t)(32 * mt + 8 * g + 4 * hi) * 2, 0, 0);
       }
     }
     if (hi == 0) {
@@ -935,6 +954,7 @@ hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
   kp.c = a.c;
   kp.vscale = a.vscale;
   kp.qmode = a.qmode;
+  kp.layout = a.layout;
   // head dimensions (d_qk, d_v): 64/64, 128/128, 192/128; FP8: 128/128
   const int dims = a.d == 64 ? 0 : (a.d == 128 ? 1 : 2);
   const int key = a.dtype == 2 ? 12 + a.causal : dims * 4 + a.dtype * 2 + a.causal;

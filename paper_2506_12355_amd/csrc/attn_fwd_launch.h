@@ -30,6 +30,7 @@ struct AttnArgs {
   float c;      // |scale| * log2(e) (FP8: |scale * q_scale * k_scale| * log2(e)), normal, > 0
   float vscale; // factor applied to O: 1, or the FP8 value scale
   int qmode;    // QMode
+  int layout;   // 0: [B][heads][N][width], 1: [B][N][heads][width] (q, k, v, o)
 };
 
 // Enqueues the kernel instance for (d, dv, dtype, causal).  Arguments have been

@@ -36,7 +36,7 @@ constexpr int kFp8 = 2;   // internal dtype code: FP8 E4M3 inputs, bf16 output
 // E4M3 codes scaled by qs, ks, vs, and o is bf16.
 int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H,
              int Hkv, int N, int d, int dv, float scale, int causal, hipStream_t stream,
-             int dtype, float qs = 1.0f, float ks = 1.0f, float vs = 1.0f) {
+             int dtype, float qs = 1.0f, float ks = 1.0f, float vs = 1.0f, int layout = QM_BHND) {
   if (!q || !k || !v || !o || !lse) return QM_ERR_NULL;
   if (B < 1 || H < 1 || N < 1 || Hkv < 1 || Hkv > H || H % Hkv != 0) return QM_ERR_SHAPE;
   if (!((d == 64 && dv == 64) || (d == 128 && dv == 128) || (d == 192 && dv == 128)))
@@ -57,6 +57,16 @@ int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, i
   if (!finite_bits(scale) || !finite_bits(qs) || !finite_bits(ks) || !finite_bits(vs))
     return QM_ERR_SCALE;
   if (causal != 0 && causal != 1) return QM_ERR_CAUSAL;
+  // QM_BNHD: head dimensions 64 and 128 (the kernels for 192-wide keys read
+  // contiguous heads only)
+  if (layout != QM_BHND && !(layout == QM_BNHD && d == dv)) return QM_ERR_LAYOUT;
+  if (layout == QM_BNHD) {
+    // rows of one head are max(H, Hkv) rows apart: the kernels' 32-bit byte
+    // offsets, including the padded last query block, must still fit
+    const uint64_t heads = (uint64_t)(H > Hkv ? H : Hkv);
+    const uint64_t row = heads * (uint64_t)d * (dtype == kFp8 ? 1u : 2u);
+    if ((uint64_t)(N + 256) * row >= (1ull << 32)) return QM_ERR_SHAPE;
+  }
 
   const size_t es = dtype == kFp8 ? 1 : 2;   // bytes per q, k, v element
   const size_t q_bytes = (size_t)(bh * nd) * es;
@@ -103,6 +113,7 @@ int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, i
   } else {
     a.qmode = qk < 0.0 ? qm::kQNegate : qm::kQNormal;
   }
+  a.layout = layout;
   return qm::launch_attn_fwd(a, stream) == hipSuccess ? QM_OK : QM_ERR_LAUNCH;
 }
 
@@ -137,6 +148,14 @@ extern "C" int qm_attn_fwd_mla(const void* q, const void* k, const void* v, void
                   dtype == kFp8 ? -1 : dtype);   // FP8 has its own entry point
 }
 
+extern "C" int qm_attn_fwd_layout(const void* q, const void* k, const void* v, void* o,
+                                  float* lse, int B, int H, int Hkv, int N, int d_qk, int d_v,
+                                  float scale, int causal, hipStream_t stream, int dtype,
+                                  int layout) {
+  return attn_fwd(q, k, v, o, lse, B, H, Hkv, N, d_qk, d_v, scale, causal, stream,
+                  dtype == kFp8 ? -1 : dtype, 1.0f, 1.0f, 1.0f, layout);
+}
+
 extern "C" const char* qm_attn_strerror(int status) {
   switch (status) {
     case QM_OK: return "success";
@@ -151,6 +170,8 @@ extern "C" const char* qm_attn_strerror(int status) {
     case QM_ERR_CAUSAL: return "causal must be 0 or 1";
     case QM_ERR_LAUNCH: return "the HIP runtime rejected the kernel launch";
     case QM_ERR_UNSUPPORTED: return "tensor pointers must be 16-byte aligned";
+    case QM_ERR_LAYOUT:
+      return "layout must be QM_BHND (0), or QM_BNHD (1) with head dimension 64 or 128";
   }
   return "unknown status";
 }

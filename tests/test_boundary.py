@@ -37,7 +37,7 @@ def _declared_functions():
 
 
 def test_header_declares_entry_points():
-    assert {"qm_attn_fwd", "qm_attn_fwd_gqa", "qm_attn_fwd_mla", "qm_attn_fwd_fp8",
+    assert {"qm_attn_fwd", "qm_attn_fwd_gqa", "qm_attn_fwd_mla", "qm_attn_fwd_fp8", "qm_attn_fwd_layout",
             "qm_attn_strerror"} <= set(_declared_functions())
 
 
@@ -172,6 +172,36 @@ def test_mla_invalid_arguments_are_rejected(lib, d_qk, d_v, over, status):
 
 def test_plain_entry_rejects_the_mla_head(lib):
     assert call(d=192) == qa.QM_ERR_HEADDIM
+
+
+def call_layout(layout, Hkv=None, d_v=None, **over):
+    a = dict(GOOD)
+    a.update(over)
+    return qa.qm_attn_fwd_layout(a["q"], a["k"], a["v"], a["o"], a["lse"], a["B"], a["H"],
+                                 a["H"] if Hkv is None else Hkv, a["N"], a["d"],
+                                 a["d"] if d_v is None else d_v, a["scale"], a["causal"],
+                                 a["stream"], a["dtype"], layout)
+
+
+@pytest.mark.parametrize("layout,kw,status", [
+    (2, {}, qa.QM_ERR_LAYOUT),
+    (-1, {}, qa.QM_ERR_LAYOUT),
+    (qa.QM_BNHD, dict(d=192, d_v=128), qa.QM_ERR_LAYOUT),      # 192-wide keys: [B][H][N][d] only
+    # a head's rows 64 heads apart: (N + 256) * 64 * 128 * 2 bytes overflow 32 bits
+    (qa.QM_BNHD, dict(N=1 << 20, H=64, d=128), qa.QM_ERR_SHAPE),
+    (qa.QM_BNHD, dict(N=1 << 20, H=64, d=128, q=None), qa.QM_ERR_NULL),   # NULL comes first
+    (qa.QM_BHND, dict(d=96), qa.QM_ERR_HEADDIM),
+    (qa.QM_BNHD, dict(causal=3), qa.QM_ERR_CAUSAL),
+    (qa.QM_BNHD, dict(Hkv=3), qa.QM_ERR_SHAPE),                # 3 does not divide H = 2
+    (qa.QM_BNHD, dict(o=Q + 2), qa.QM_ERR_ALIAS),
+    (qa.QM_BNHD, dict(k=K + 8), qa.QM_ERR_UNSUPPORTED),
+], ids=lambda x: str(x))
+def test_layout_entry_rejects_invalid_arguments(lib, layout, kw, status):
+    assert call_layout(layout, **kw) == status
+
+
+def test_layout_error_text(lib):
+    assert "QM_BNHD" in qa.strerror(qa.QM_ERR_LAYOUT)
 
 
 def call_fp8(qs=0.01, ks=0.01, vs=0.01, **over):
