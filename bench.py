@@ -23,7 +23,9 @@ Prints one JSON line.  Extra objects:
                 once the kernel source has changed since those counters were
                 taken;
   cpu_baseline  the fp64 CPU oracle timed on this host on a bounded sample of
-                the same workload (whole heads, both masks), in the same unit.
+                the same workload (whole heads, both masks), in the same unit;
+  cpu_single_core  the oracle on one core over the two small workloads
+                (B=1 H=2 N=128 d=64 and B=8 H=16 N=1024 d=64, fp16, unmasked).
 """
 from __future__ import annotations
 
@@ -177,6 +179,24 @@ def cpu_baseline(w, q, k, v, max_workers=16, descale=None):
                    f"spread over {cores} processes with single-threaded BLAS on {model}; "
                    f"wall {wall:.1f} s"),
     }
+
+
+def cpu_single_core(names=("mha_b1_h2_n128_d64_f16", "mha_b8_h16_n1024_d64_f16")):
+    """The oracle on one core (single-threaded BLAS) over whole small workloads,
+    unmasked: seconds and fp64 GFLOP/s by the metric's count."""
+    from threadpoolctl import threadpool_limits
+    from oracle import attention_fp64
+    out = {}
+    for name in names:
+        w = si.WORKLOADS[name]
+        q, k, v = w.inputs()
+        with threadpool_limits(limits=1):
+            t0 = time.perf_counter()
+            attention_fp64(q, k, v, w.scale, False, w.dtype)
+            dt = time.perf_counter() - t0
+        out[name] = {"seconds": round(dt, 4),
+                     "gflops": round(flops(w.B, w.H, w.N, w.d, False) / dt / 1e9, 3)}
+    return out
 
 
 # --------------------------------------------------------------------------
@@ -388,6 +408,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, q, k, v, descale=scales)
+        result["cpu_single_core"] = cpu_single_core()
     print(json.dumps(result), flush=True)
 
 
