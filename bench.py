@@ -267,7 +267,7 @@ def main():
     ap.add_argument("--workload", default=si.BENCH_WORKLOAD, choices=sorted(si.WORKLOADS),
                     help="named workload (default: the one the metric is quoted on)")
     ap.add_argument("--layout", default="bhnd", choices=("bhnd", "bnhd"),
-                    help="memory layout of q, k, v and o for 16-bit workloads: [B][H][N][d] "
+                    help="memory layout of q, k, v and o: [B][H][N][d] "
                          "(default) or [B][N][H][d]")
     ap.add_argument("--grid", action="store_true",
                     help="measure the paper's benchmark grid instead (one JSON line per shape; "
@@ -304,17 +304,16 @@ def main():
         # E4M3 codes with per-tensor scales; the output is bf16
         q, k, v, scales = w.fp8_inputs()
         tdtype = torch.bfloat16
-        tq, tk, tv = (torch.from_numpy(x).to(dev).view(torch.float8_e4m3fn) for x in (q, k, v))
+        tq, tk, tv = (torch.from_numpy(x).to(dev) for x in (q, k, v))   # uint8 codes
     else:
         q, k, v = w.inputs()
         scales = None
         tdtype = torch.bfloat16 if w.dtype == "bf16" else torch.float16
         tq, tk, tv = (torch.from_numpy(x.view(np.int16)).to(dev).view(tdtype) for x in (q, k, v))
-        if args.layout == "bnhd":
-            tq, tk, tv = (t.transpose(1, 2).contiguous() for t in (tq, tk, tv))
-    if fp8 and args.layout != "bhnd":
-        print("the FP8 entry point takes [B][H][N][d] only", file=sys.stderr)
-        sys.exit(2)
+    if args.layout == "bnhd":
+        tq, tk, tv = (t.transpose(1, 2).contiguous() for t in (tq, tk, tv))
+    if fp8:
+        tq, tk, tv = (t.view(torch.float8_e4m3fn) for t in (tq, tk, tv))
     peak = PEAK_TFLOPS_FP8 if fp8 else PEAK_TFLOPS
     peak_per_clk = PEAK_FLOP_PER_CLK_FP8 if fp8 else PEAK_FLOP_PER_CLK
     masks = list(w.causal)
@@ -330,7 +329,7 @@ def main():
                 ev[m].record(stream)
             if fp8:
                 qa.fwd_fp8(tq, tk, tv, scales, causal=causal, scale=w.scale, out=outs[m][0],
-                           lse=outs[m][1], stream=stream)
+                           lse=outs[m][1], stream=stream, layout=args.layout)
             else:
                 qa.fwd(tq, tk, tv, causal=causal, scale=w.scale, out=outs[m][0],
                        lse=outs[m][1], stream=stream, layout=args.layout)

@@ -43,7 +43,7 @@ typedef enum {
   QM_BF16 = 1  /* bfloat16 (top half of an IEEE binary32) */
 } qm_dtype_t;
 
-/* Memory layouts of q, k, v and o (qm_attn_fwd_layout; lse is always [B][H][N]). */
+/* Memory layouts of q, k, v and o (the _layout entry points; lse is always [B][H][N]). */
 typedef enum {
   QM_BHND = 0,  /* [B][heads][N][width]: each head a contiguous N x width slab */
   QM_BNHD = 1   /* [B][N][heads][width]: each token's heads side by side */
@@ -193,6 +193,19 @@ int qm_attn_fwd_fp8(const void* q, const void* k, const void* v, void* o, float*
 int qm_attn_fwd_layout(const void* q, const void* k, const void* v, void* o, float* lse,
                        int B, int H, int Hkv, int N, int d_qk, int d_v, float scale,
                        int causal, hipStream_t stream, int dtype, int layout);
+
+/*
+ * qm_attn_fwd_fp8_layout - qm_attn_fwd_fp8 with grouped-query key/value heads
+ * and the memory layout as arguments: k and v hold Hkv heads (H % Hkv == 0;
+ * query head h reads key/value head h / (H / Hkv), as in qm_attn_fwd_gqa),
+ * and q, k, v and o are stored as `layout` (QM_BHND or QM_BNHD, as in
+ * qm_attn_fwd_layout).  The arithmetic, its error bound and the status codes
+ * are those of qm_attn_fwd_fp8.
+ */
+int qm_attn_fwd_fp8_layout(const void* q, const void* k, const void* v, void* o, float* lse,
+                           int B, int H, int Hkv, int N, int d, float q_scale, float k_scale,
+                           float v_scale, float scale, int causal, hipStream_t stream,
+                           int layout);
 
 /* qm_attn_strerror - a static, human-readable string for a status code. */
 const char* qm_attn_strerror(int status);

@@ -4,7 +4,7 @@
 per-row log-sum-exp for [B, H, N, d] fp16/bf16 tensors on one GPU; k and v may
 have fewer heads than q (grouped-query and multi-query attention), and v a
 narrower head than q and k (the MLA shape, 192/128).  ``fwd_fp8`` takes FP8
-(E4M3) inputs with per-tensor scales; ``fwd(..., layout="bnhd")`` takes
+(E4M3) inputs with per-tensor scales, also with fewer key/value heads; ``fwd(..., layout="bnhd")`` takes
 [B, N, heads, d] tensors.  The
 operation and its arguments are documented in ``include/qm_attn.h``.
 """
@@ -31,6 +31,7 @@ from .binding import (  # noqa: F401
     load_library,
     qm_attn_fwd,
     qm_attn_fwd_fp8,
+    qm_attn_fwd_fp8_layout,
     qm_attn_fwd_gqa,
     qm_attn_fwd_layout,
     qm_attn_fwd_mla,

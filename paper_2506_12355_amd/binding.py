@@ -88,6 +88,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
             ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
         ]
         lib.qm_attn_fwd_layout.restype = ctypes.c_int
+        lib.qm_attn_fwd_fp8_layout.argtypes = [
+            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+            ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+            ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_int,
+            ctypes.c_void_p, ctypes.c_int,
+        ]
+        lib.qm_attn_fwd_fp8_layout.restype = ctypes.c_int
         lib.qm_attn_strerror.argtypes = [ctypes.c_int]
         lib.qm_attn_strerror.restype = ctypes.c_char_p
         _lib = lib
@@ -134,28 +141,44 @@ def qm_attn_fwd_fp8(q, k, v, o, lse, B, H, N, d, q_scale, k_scale, v_scale, scal
 
 
 def fwd_fp8(q, k, v, scales, causal: bool = False, scale: float | None = None, out=None,
-            lse=None, stream=None):
-    """FP8 attention forward: q, k, v are [B, H, N, d] tensors of OCP E4M3 codes
-    (``torch.float8_e4m3fn`` or ``uint8``) on a ROCm device, ``scales`` the three
-    per-tensor factors (q_scale, k_scale, v_scale).  Returns (o, lse): o bf16
-    [B, H, N, d], lse float32 [B, H, N].  ``scale`` defaults to 1/sqrt(d)
-    rounded to float32."""
+            lse=None, stream=None, layout: str = "bhnd"):
+    """FP8 attention forward: q is [B, H, N, d], k and v [B, Hkv, N, d] (Hkv
+    dividing H: grouped-query attention when Hkv < H) tensors of OCP E4M3 codes
+    (``torch.float8_e4m3fn`` or ``uint8``) on a ROCm device; ``scales`` holds
+    the three per-tensor factors (q_scale, k_scale, v_scale).  With
+    ``layout="bnhd"`` the tensors are [B, N, heads, d] instead.  Returns
+    (o, lse): o bf16 shaped like q, lse float32 [B, H, N] in either layout.
+    ``scale`` defaults to 1/sqrt(d) rounded to float32.  Multi-head
+    [B, H, N, d] calls go to ``qm_attn_fwd_fp8``, the others to
+    ``qm_attn_fwd_fp8_layout``."""
     import torch
 
+    if layout not in ("bhnd", "bnhd"):
+        raise ValueError(f"layout must be 'bhnd' or 'bnhd', not {layout!r}")
+    bnhd = layout == "bnhd"
+    names = "[B, N, H, d]" if bnhd else "[B, H, N, d]"
+
+    def shape(t):   # (B, heads, N, d) whatever the layout
+        s = tuple(t.shape)
+        return (s[0], s[2], s[1], s[3]) if bnhd else s
+
     for t in (q, k, v):
-        if t.dim() != 4 or t.shape != q.shape:
-            raise ValueError("q, k and v must share the shape [B, H, N, d]")
+        if t.dim() != 4:
+            raise ValueError(f"q, k and v must have shape {names}")
         if t.dtype not in (torch.uint8, torch.float8_e4m3fn):
             raise TypeError("FP8 inputs must be float8_e4m3fn or uint8 codes")
         if not t.is_cuda or t.device != q.device or not t.is_contiguous():
             raise ValueError("q, k and v must be contiguous tensors on one ROCm device")
-    B, H, N, d = q.shape
+    if shape(v) != shape(k) or shape(k)[0] != shape(q)[0] or shape(k)[2:] != shape(q)[2:]:
+        raise ValueError("k and v must hold Hkv heads matching q in B, N and d")
+    B, H, N, d = shape(q)
+    Hkv = shape(k)[1]
     if scale is None:
         scale = float(torch.tensor(1.0 / d ** 0.5, dtype=torch.float32))
     if out is None:
-        out = torch.empty((B, H, N, d), dtype=torch.bfloat16, device=q.device)
+        out = torch.empty(tuple(q.shape), dtype=torch.bfloat16, device=q.device)
     elif out.shape != q.shape or out.dtype != torch.bfloat16 or not out.is_contiguous():
-        raise ValueError("out must be a contiguous bfloat16 tensor like q")
+        raise ValueError("out must be a contiguous bfloat16 tensor shaped like q")
     if lse is None:
         lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
     elif lse.shape != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous():
@@ -164,12 +187,27 @@ def fwd_fp8(q, k, v, scales, causal: bool = False, scale: float | None = None, o
         stream = torch.cuda.current_stream(q.device)
     qs, ks, vs = (float(t) for t in scales)
     with torch.cuda.device(q.device):
-        status = qm_attn_fwd_fp8(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
-                                 lse.data_ptr(), B, H, N, d, qs, ks, vs, scale,
-                                 1 if causal else 0, stream.cuda_stream)
+        if bnhd or Hkv != H:
+            status = qm_attn_fwd_fp8_layout(q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                                            out.data_ptr(), lse.data_ptr(), B, H, Hkv, N, d,
+                                            qs, ks, vs, scale, 1 if causal else 0,
+                                            stream.cuda_stream, QM_BNHD if bnhd else QM_BHND)
+        else:
+            status = qm_attn_fwd_fp8(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                     lse.data_ptr(), B, H, N, d, qs, ks, vs, scale,
+                                     1 if causal else 0, stream.cuda_stream)
     if status != QM_OK:
         raise QmAttnError(status, strerror(status))
     return out, lse
+
+
+def qm_attn_fwd_fp8_layout(q, k, v, o, lse, B, H, Hkv, N, d, q_scale, k_scale, v_scale, scale,
+                           causal, stream, layout) -> int:
+    """The general FP8 C entry point (key/value heads and layout as arguments)
+    with plain integers for pointers; returns the status."""
+    return load_library().qm_attn_fwd_fp8_layout(
+        q, k, v, o, lse, int(B), int(H), int(Hkv), int(N), int(d), float(q_scale),
+        float(k_scale), float(v_scale), float(scale), int(causal), stream, int(layout))
 
 
 def _dtype_code(t) -> int:

@@ -156,6 +156,14 @@ extern "C" int qm_attn_fwd_layout(const void* q, const void* k, const void* v, v
                   dtype == kFp8 ? -1 : dtype, 1.0f, 1.0f, 1.0f, layout);
 }
 
+extern "C" int qm_attn_fwd_fp8_layout(const void* q, const void* k, const void* v, void* o,
+                                      float* lse, int B, int H, int Hkv, int N, int d,
+                                      float q_scale, float k_scale, float v_scale, float scale,
+                                      int causal, hipStream_t stream, int layout) {
+  return attn_fwd(q, k, v, o, lse, B, H, Hkv, N, d, d, scale, causal, stream, kFp8, q_scale,
+                  k_scale, v_scale, layout);
+}
+
 extern "C" const char* qm_attn_strerror(int status) {
   switch (status) {
     case QM_OK: return "success";

@@ -104,15 +104,17 @@ def f32_to_e4m3_bits(x: np.ndarray) -> np.ndarray:
     return np.where(np.signbit(x32), code | np.uint8(0x80), code).astype(np.uint8)   # keeps -0
 
 
-def make_qkv_fp8(B: int, H: int, N: int, d: int, seed: int = 0):
+def make_qkv_fp8(B: int, H: int, N: int, d: int, seed: int = 0, Hkv: int | None = None):
     """FP8 inputs: Q, K, V drawn as ``make_qkv`` draws them (fp32 normals, Q then
-    K then V), each scaled per tensor so that its largest magnitude maps to 448,
-    rounded to E4M3.  Returns (q8, k8, v8, scales) with uint8 codes and the three
-    float32 descale factors: the real tensor is scale * decode(code)."""
+    K then V; K and V with ``Hkv`` heads, default H), each scaled per tensor so
+    that its largest magnitude maps to 448, rounded to E4M3.  Returns (q8, k8,
+    v8, scales) with uint8 codes and the three float32 descale factors: the
+    real tensor is scale * decode(code)."""
+    Hkv = H if Hkv is None else Hkv
     rng = np.random.default_rng(seed)
     out, scales = [], []
-    for _ in ("q", "k", "v"):
-        x = rng.standard_normal((B, H, N, d), dtype=np.float32)
+    for heads in (H, Hkv, Hkv):
+        x = rng.standard_normal((B, heads, N, d), dtype=np.float32)
         s = np.float32(np.max(np.abs(x)) / np.float32(E4M3_MAX))
         y = np.minimum(np.abs(x / s), np.float32(E4M3_MAX)) * np.sign(x)
         out.append(f32_to_e4m3_bits(y))
@@ -122,26 +124,27 @@ def make_qkv_fp8(B: int, H: int, N: int, d: int, seed: int = 0):
 
 
 def make_qkv_fp8_dyadic(B: int, H: int, N: int, d: int, seed: int = 0,
-                        v_binade: bool = False):
+                        v_binade: bool = False, Hkv: int | None = None):
     """FP8 inputs with small integer dot products.  Each Q row holds +1 or -1
     (even odds) at two distinct columns drawn uniformly and zeros elsewhere; K
     entries are integers drawn uniformly from -2 .. 2; V holds codes drawn
     uniformly from the 254 finite E4M3 codes (every exponent, subnormals and
     both zeros included), or with ``v_binade`` from the 16 codes of [1, 2)
     and (-2, -1] (random sign and mantissa).  Every q . k is then an integer
-    in [-4, 4].  Returns uint8 codes (q8, k8, v8); the caller picks the scale
-    factors."""
+    in [-4, 4].  K and V have ``Hkv`` heads (default H).  Returns uint8 codes
+    (q8, k8, v8); the caller picks the scale factors."""
+    Hkv = H if Hkv is None else Hkv
     rng = np.random.default_rng(seed)
     cols = np.argsort(rng.random((B, H, N, d)), axis=-1)[..., :2]
     signs = rng.choice(np.array([-1.0, 1.0], dtype=np.float32), size=(B, H, N, 2))
     q = np.zeros((B, H, N, d), dtype=np.float32)
     np.put_along_axis(q, cols, signs, axis=-1)
-    k = rng.integers(-2, 3, size=(B, H, N, d)).astype(np.float32)
+    k = rng.integers(-2, 3, size=(B, Hkv, N, d)).astype(np.float32)
     if v_binade:
         pool = np.array([s << 7 | 7 << 3 | m for s in (0, 1) for m in range(8)], dtype=np.uint8)
     else:
         pool = np.array([c for c in range(256) if c & 0x7F != 0x7F], dtype=np.uint8)
-    v = pool[rng.integers(0, pool.size, size=(B, H, N, d))]
+    v = pool[rng.integers(0, pool.size, size=(B, Hkv, N, d))]
     return f32_to_e4m3_bits(q), f32_to_e4m3_bits(k), v
 
 
@@ -185,7 +188,7 @@ class Workload:
 
     def fp8_inputs(self):
         """(q8, k8, v8, (q_scale, k_scale, v_scale)) of an FP8 workload."""
-        return make_qkv_fp8(self.B, self.H, self.N, self.d, seed=self.seed)
+        return make_qkv_fp8(self.B, self.H, self.N, self.d, seed=self.seed, Hkv=self.kv_heads)
 
 
 WORKLOADS = {
@@ -220,6 +223,10 @@ WORKLOADS = {
         # FP8 table is MHA with the causal mask at d = 128
         Workload("fp8_b2_h32_n8192_d128", 2, 32, 8192, 128, "e4m3", (False, True)),
         Workload("fp8_b2_h3_n333_d128", 2, 3, 333, 128, "e4m3", (False, True)),
+        # FP8 with the appendix's grouped-query heads (64 query / 8 key-value)
+        Workload("fp8_gqa_b2_h64_kv8_n8192_d128_causal", 2, 64, 8192, 128, "e4m3", (True,),
+                 Hkv=8),
+        Workload("fp8_gqa_b2_h6_kv2_n555_d128", 2, 6, 555, 128, "e4m3", (False, True), Hkv=2),
     )
 }
 

@@ -37,7 +37,8 @@ def _declared_functions():
 
 
 def test_header_declares_entry_points():
-    assert {"qm_attn_fwd", "qm_attn_fwd_gqa", "qm_attn_fwd_mla", "qm_attn_fwd_fp8", "qm_attn_fwd_layout",
+    assert {"qm_attn_fwd", "qm_attn_fwd_gqa", "qm_attn_fwd_mla", "qm_attn_fwd_fp8",
+            "qm_attn_fwd_layout", "qm_attn_fwd_fp8_layout",
             "qm_attn_strerror"} <= set(_declared_functions())
 
 
@@ -234,10 +235,53 @@ def test_fp8_invalid_arguments_are_rejected(lib, kw, status):
     assert call_fp8(qs, ks, vs, **kw) == status
 
 
+def call_fp8_layout(layout, Hkv=None, qs=0.01, ks=0.01, vs=0.01, **over):
+    a = dict(GOOD, d=128)
+    a.update(over)
+    return qa.qm_attn_fwd_fp8_layout(a["q"], a["k"], a["v"], a["o"], a["lse"], a["B"], a["H"],
+                                     a["H"] if Hkv is None else Hkv, a["N"], a["d"], qs, ks, vs,
+                                     a["scale"], a["causal"], a["stream"], layout)
+
+
+@pytest.mark.parametrize("layout,kw,status", [
+    (2, {}, qa.QM_ERR_LAYOUT),
+    (-1, dict(Hkv=1), qa.QM_ERR_LAYOUT),
+    (qa.QM_BNHD, dict(d=64), qa.QM_ERR_HEADDIM),          # FP8 runs at d = 128 only
+    (qa.QM_BHND, dict(d=192), qa.QM_ERR_HEADDIM),
+    (qa.QM_BHND, dict(Hkv=0), qa.QM_ERR_SHAPE),
+    (qa.QM_BNHD, dict(Hkv=3), qa.QM_ERR_SHAPE),           # 3 does not divide H = 2
+    (qa.QM_BNHD, dict(Hkv=4), qa.QM_ERR_SHAPE),           # more key/value heads than query heads
+    (qa.QM_BNHD, dict(v=None), qa.QM_ERR_NULL),
+    (qa.QM_BNHD, dict(vs=float("nan")), qa.QM_ERR_SCALE),
+    (qa.QM_BHND, dict(Hkv=1, qs=3e38, ks=3e38), qa.QM_ERR_SCALE),
+    (qa.QM_BNHD, dict(causal=5), qa.QM_ERR_CAUSAL),
+    # B=1, H=2, Hkv=1, N=128, d=128: k spans 16 KiB of one-byte codes
+    (qa.QM_BHND, dict(Hkv=1, o=K + 8 * 1024), qa.QM_ERR_ALIAS),
+    (qa.QM_BNHD, dict(Hkv=1, lse=L + 4), qa.QM_ERR_UNSUPPORTED),
+], ids=lambda x: str(x))
+def test_fp8_layout_entry_rejects_invalid_arguments(lib, layout, kw, status):
+    kw = dict(kw)
+    Hkv = kw.pop("Hkv", None)
+    assert call_fp8_layout(layout, Hkv, **kw) == status
+
+
+def test_fp8_layout_row_bound_counts_one_byte_codes(lib):
+    """[B][N][H][d] rows of one-byte codes are half as wide as 16-bit ones, so
+    N = 2^18 with 64 heads of 128 fits the kernels' 32-bit offsets in FP8
+    (the call gets as far as the alignment check) but not in bf16."""
+    T = 1 << 40
+    big = dict(q=T, k=2 * T, v=3 * T, o=4 * T, lse=5 * T + 4, N=1 << 18, H=64, d=128)
+    assert call_fp8_layout(qa.QM_BNHD, **big) == qa.QM_ERR_UNSUPPORTED
+    assert call_fp8_layout(qa.QM_BNHD, **dict(big, N=1 << 19)) == qa.QM_ERR_SHAPE
+    assert call_layout(qa.QM_BNHD, **dict(big, dtype=qa.QM_BF16)) == qa.QM_ERR_SHAPE
+    assert call_layout(qa.QM_BHND, **dict(big, dtype=qa.QM_BF16)) == qa.QM_ERR_UNSUPPORTED
+
+
 def test_16bit_entries_reject_the_fp8_code(lib):
     assert call(dtype=2) == qa.QM_ERR_DTYPE
     assert call_gqa(1, H=2, dtype=2) == qa.QM_ERR_DTYPE
     assert call_mla(128, 128, dtype=2) == qa.QM_ERR_DTYPE
+    assert call_layout(qa.QM_BHND, dtype=2) == qa.QM_ERR_DTYPE
 
 
 def test_inputs_may_alias_each_other(lib):

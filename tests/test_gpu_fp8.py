@@ -1,5 +1,7 @@
-"""GPU parity for the FP8 forward (``qm_attn_fwd_fp8``): OCP E4M3 inputs with
-per-tensor scale factors, bf16 output, head dimension 128.
+"""GPU parity for the FP8 forward (``qm_attn_fwd_fp8``, and
+``qm_attn_fwd_fp8_layout`` for fewer key/value heads and the [B][N][H][d]
+layout): OCP E4M3 inputs with per-tensor scale factors, bf16 output, head
+dimension 128.
 
 Two roundings separate the kernel from the exact definition on general
 inputs.
@@ -185,12 +187,14 @@ def _rounding_bound(q8, k8, v8, scales, scale, causal, rows, O, Or):
     scale64 = float(np.float32(scale))
     cnat = abs(scale64 * sq * sk)
     bound = np.empty_like(Or)
+    group = q8.shape[1] // k8.shape[1]   # query heads per key/value head
     heads = {}
     for idx, (b, h, i) in enumerate(rows):
-        if (b, h) not in heads:
-            K8 = decode_fp64(k8[b, h], "e4m3")
-            heads = {(b, h): (K8 * sk, np.abs(K8), np.abs(decode_fp64(v8[b, h], "e4m3")) * sv)}
-        K, Ka, Va = heads[(b, h)]
+        hk = h // group
+        if (b, hk) not in heads:
+            K8 = decode_fp64(k8[b, hk], "e4m3")
+            heads = {(b, hk): (K8 * sk, np.abs(K8), np.abs(decode_fp64(v8[b, hk], "e4m3")) * sv)}
+        K, Ka, Va = heads[(b, hk)]
         Q8 = decode_fp64(q8[b, h, i:i + 1], "e4m3")
         S = scores_fp64(Q8 * sq, K, scale64, causal, row0=i)
         P, _ = softmax_rows_fp64(S)
@@ -370,3 +374,143 @@ def test_fp8_general_inputs_edge_lengths(qa, N):
         Of, Orf = O.reshape(-1, 128), Or.reshape(-1, 128)
         bound = _rounding_bound(q8, k8, v8, scales, scale, causal, rows, Of, Orf)
         _gate(Of, lse.ravel(), Orf, lr.ravel(), bound, f"FP8 general N={N} causal={causal}")
+
+
+# -------------------------------------------------- grouped-query heads, [B][N][H][d]
+def _bnhd(x):
+    """[B][heads][N][d] array -> contiguous [B][N][heads][d]."""
+    return np.ascontiguousarray(np.swapaxes(x, 1, 2))
+
+
+def _run_any(qa, q8, k8, v8, scales, causal, scale, layout):
+    """fwd_fp8 on [B][H][N][d] codes stored in ``layout``; returns the device
+    outputs with o in [B][H][N][d] order."""
+    import torch
+    lay = _bnhd if layout == "bnhd" else (lambda x: x)
+    o, lse = qa.fwd_fp8(*(_codes(lay(x)) for x in (q8, k8, v8)), scales, causal=causal,
+                        scale=scale, layout=layout)
+    torch.cuda.synchronize()
+    if layout == "bnhd":
+        o = o.transpose(1, 2).contiguous()
+    return o, lse
+
+
+def _same_as_multi_head(qa, o, lse, q8, k8, v8, scales, causal, scale):
+    """Byte-identical to the multi-head [B][H][N][d] call with each key/value
+    head repeated for its query heads (same arithmetic, other addresses)."""
+    import torch
+    g = q8.shape[1] // k8.shape[1]
+    ob, lb = _run_any(qa, q8, np.repeat(k8, g, axis=1), np.repeat(v8, g, axis=1), scales,
+                      causal, scale, "bhnd")
+    assert torch.equal(o.view(torch.int16), ob.view(torch.int16))
+    assert torch.equal(lse.view(torch.int32), lb.view(torch.int32))
+
+
+@pytest.mark.parametrize("layout", ["bhnd", "bnhd"])
+@pytest.mark.parametrize("H,Hkv,N", [(6, 2, 333), (4, 1, 65), (3, 3, 1000), (8, 2, 1)])
+def test_fp8_grouped_heads_and_layouts_dyadic(qa, H, Hkv, N, layout):
+    """Exact-weight inputs with H query and Hkv key/value heads in either
+    layout: the oracle's value up to fp32 summation and the bf16 rounding."""
+    q8, k8, v8 = si.make_qkv_fp8_dyadic(2, H, N, 128, seed=70 + H + N, v_binade=True, Hkv=Hkv)
+    scales = (0.5, 2.0, 0.0123)
+    for causal in (False, True):
+        what = f"FP8 {layout} H={H} Hkv={Hkv} N={N} causal={causal}"
+        _say(f"case {what}")
+        o, lse = _run_any(qa, q8, k8, v8, scales, causal, LN2, layout)
+        O, L = to_host64(o), to_host64(lse)
+        Or, lr = attention_fp64(q8, k8, v8, LN2, causal, "e4m3", descale=scales)
+        PV, _ = attention_fp64(q8, k8, v8 & 0x7F, LN2, causal, "e4m3", descale=scales)
+        bound = np.maximum(half_ulp(Or, "bf16"), half_ulp(O, "bf16")) + _summation(N) * PV
+        _gate(O, L, Or, lr, bound, what)
+        _same_as_multi_head(qa, o, lse, q8, k8, v8, scales, causal, LN2)
+
+
+@pytest.mark.parametrize("layout", ["bhnd", "bnhd"])
+def test_fp8_grouped_workload_full(qa, layout):
+    """General FP8 inputs, 6 query / 2 key-value heads, N = 555, in full under
+    the rounding bound."""
+    w = si.WORKLOADS["fp8_gqa_b2_h6_kv2_n555_d128"]
+    q8, k8, v8, scales = w.fp8_inputs()
+    assert k8.shape == (w.B, w.kv_heads, w.N, w.d)
+    rows = [(b, h, i) for b in range(w.B) for h in range(w.H) for i in range(w.N)]
+    for causal in w.causal:
+        what = f"{w.name} {layout} causal={causal}"
+        _say(f"case {what}")
+        o, lse = _run_any(qa, q8, k8, v8, scales, causal, w.scale, layout)
+        O, L = to_host64(o), to_host64(lse)
+        Or, lr = attention_fp64(q8, k8, v8, w.scale, causal, "e4m3", descale=scales)
+        Of, Orf = O.reshape(-1, w.d), Or.reshape(-1, w.d)
+        bound = _rounding_bound(q8, k8, v8, scales, w.scale, causal, rows, Of, Orf)
+        _gate(Of, L.ravel(), Orf, lr.ravel(), bound, what)
+        _same_as_multi_head(qa, o, lse, q8, k8, v8, scales, causal, w.scale)
+
+
+def test_fp8_grouped_long_workload_sampled(qa):
+    """64 query / 8 key-value heads, N = 8192, causal, on sampled rows."""
+    import torch
+    w = si.WORKLOADS["fp8_gqa_b2_h64_kv8_n8192_d128_causal"]
+    _say(f"case {w.name}: drawing inputs")
+    q8, k8, v8, scales = w.fp8_inputs()
+    _say(f"case {w.name}: running")
+    o, lse = qa.fwd_fp8(_codes(q8), _codes(k8), _codes(v8), scales, causal=True, scale=w.scale)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(o).all()) and bool(torch.isfinite(lse).all())
+    rows = sorted(_sample_rows(w, 64, seed=71))
+    ix = tuple(torch.tensor(np.array(rows).T).cuda())
+    O, L = to_host64(o[ix]), to_host64(lse[ix])
+    Or, lr = attention_rows_fp64(q8, k8, v8, w.scale, True, "e4m3", rows, descale=scales)
+    bound = _rounding_bound(q8, k8, v8, scales, w.scale, True, rows, O, Or)
+    _gate(O, L, Or, lr, bound, f"{w.name} sampled rows")
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_fp8_bnhd_bench_shape_matches_bhnd(qa, long_inputs, causal):
+    """The FP8 benchmark shape (B = 2, H = 32, N = 8192) stored [B][N][H][d]:
+    byte-identical to the [B][H][N][d] launch, and on sampled rows within
+    the rounding bound of the oracle."""
+    import torch
+    w, (q8, k8, v8, scales) = long_inputs
+    _say(f"case {w.name} bnhd causal={causal}")
+    o, lse = _run_any(qa, q8, k8, v8, scales, causal, w.scale, "bnhd")
+    ob, lb = _run_any(qa, q8, k8, v8, scales, causal, w.scale, "bhnd")
+    assert torch.equal(o.view(torch.int16), ob.view(torch.int16))
+    assert torch.equal(lse.view(torch.int32), lb.view(torch.int32))
+    rows = sorted(_sample_rows(w, 32, seed=72 + causal))
+    ix = tuple(torch.tensor(np.array(rows).T).cuda())
+    O, L = to_host64(o[ix]), to_host64(lse[ix])
+    Or, lr = attention_rows_fp64(q8, k8, v8, w.scale, causal, "e4m3", rows, descale=scales)
+    bound = _rounding_bound(q8, k8, v8, scales, w.scale, causal, rows, O, Or)
+    _gate(O, L, Or, lr, bound, f"{w.name} bnhd causal={causal} sampled rows")
+
+
+def test_fp8_bnhd_bounds_and_outputs(qa):
+    """[B][N][H][d] codes with NaN codes right after each input: rows past the
+    end read as zeros although a head's rows are heads x d bytes apart; a
+    NaN-poisoned output is fully overwritten and its guard zones stay."""
+    import torch
+    B, H, Hkv, N, d = 2, 4, 2, 197, 128
+    q8, k8, v8 = si.make_qkv_fp8_dyadic(B, H, N, d, seed=73, v_binade=True, Hkv=Hkv)
+    views = []
+    for x in (q8, k8, v8):
+        t = _bnhd(x).reshape(-1)
+        buf = torch.full((t.size + 2 * 64 * H * d,), 0x7F, dtype=torch.uint8, device="cuda")
+        buf[:t.size] = torch.from_numpy(t).cuda()
+        views.append(buf[:t.size].view(B, N, x.shape[1], d).view(torch.float8_e4m3fn))
+    scales = (1.0, 1.0, 0.05)
+    G = 256
+    for causal in (False, True):
+        _say(f"case FP8 bnhd guarded causal={causal}")
+        obuf = torch.full((B * N * H * d + 2 * G,), float("nan"), dtype=torch.bfloat16,
+                          device="cuda")
+        obuf[:G] = 7.0
+        obuf[-G:] = 7.0
+        o = obuf[G:G + B * N * H * d].view(B, N, H, d)
+        o, lse = qa.fwd_fp8(*views, scales, causal=causal, scale=LN2, out=o, layout="bnhd")
+        torch.cuda.synchronize()
+        assert bool(torch.isfinite(o).all()) and bool(torch.isfinite(lse).all())
+        assert bool((obuf[:G] == 7.0).all()) and bool((obuf[-G:] == 7.0).all())
+        Or, lr = attention_fp64(q8, k8, v8, LN2, causal, "e4m3", descale=scales)
+        PV, _ = attention_fp64(q8, k8, v8 & 0x7F, LN2, causal, "e4m3", descale=scales)
+        O, L = np.swapaxes(to_host64(o), 1, 2), to_host64(lse)
+        bound = np.maximum(half_ulp(Or, "bf16"), half_ulp(O, "bf16")) + _summation(N) * PV
+        _gate(O, L, Or, lr, bound, f"FP8 bnhd guarded causal={causal}")
