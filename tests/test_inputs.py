@@ -104,3 +104,65 @@ def test_dyadic_fp8_inputs_have_small_integer_scores():
     _, _, vb = si.make_qkv_fp8_dyadic(2, 3, 40, 128, seed=7, v_binade=True)
     vals = np.abs(dec(vb))
     assert vals.min() >= 1.0 and vals.max() < 2.0 and len(np.unique(vb)) == 16
+
+
+# ------------------------------------------------ the paper's benchmark setting
+def _golden_setting():
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "benchmark_setting.txt")
+    out = {}
+    for line in open(path):
+        line = line.split("#", 1)[0].strip()
+        if line:
+            key, *vals = line.split()
+            out[key] = vals
+    return out
+
+
+def test_grid_workloads_follow_the_paper_setting():
+    """The bf16 and FP8 grid workloads are the paper's stated configuration:
+    every sequence length, 16k tokens per batch, hidden 2048 split into heads
+    of 64 or 128, both masks (FP8: d = 128, causal)."""
+    g = _golden_setting()
+    seqlens = [int(x) for x in g["seqlens"]]
+    tokens, hidden = int(g["tokens_per_batch"][0]), int(g["hidden"][0])
+    assert list(si.GRID_N) == seqlens
+    assert sorted(si.GRID_D) == sorted(int(x) for x in g["head_dims"])
+    heads = {64: int(g["heads_at_head_dim_64"][0]), 128: int(g["heads_at_head_dim_128"][0])}
+    masks = {"none": False, "causal": True}
+    for d in si.GRID_D:
+        assert heads[d] * d == hidden
+        for n in seqlens:
+            w = si.GRID[f"grid_d{d}_n{n}"]
+            assert (w.B * w.N, w.H, w.d, w.kv_heads, w.d_v) == (tokens, heads[d], d, w.H, d)
+            assert set(w.causal) == {masks[m] for m in g["masks"]}
+    d8 = int(g["fp8_head_dim"][0])
+    for n in seqlens:
+        w = si.GRID_FP8[f"grid_fp8_d128_n{n}"]
+        assert (w.dtype, w.B * w.N, w.H * w.d, w.d) == ("e4m3", tokens, hidden, d8)
+        assert set(w.causal) == {masks[m] for m in g["fp8_masks"]}
+
+
+def test_flop_count_is_the_paper_formula():
+    """bench.py's count is the paper's 4 * seqlen^2 * head_dim * heads per
+    sequence (times the batch), halved under the causal mask; the MLA shape
+    counts its two products with their own head dimensions."""
+    import bench
+    g = _golden_setting()
+    factor = int(g["flops_factor"][0])
+    for w in list(si.GRID.values()):
+        f = factor * w.N ** 2 * w.d * w.H * w.B
+        assert bench.flops(w.B, w.H, w.N, w.d, False) == f
+        assert bench.flops(w.B, w.H, w.N, w.d, True) == f / 2
+    e, r = int(g["mla_embedding_dim"][0]), int(g["mla_rope_dim"][0])
+    w = si.WORKLOADS["mla_b2_h128_n8192_d192_dv128_bf16_causal"]
+    assert (w.d, w.d_v) == (e + r, e)
+    assert bench.flops(w.B, w.H, w.N, w.d, False, w.d_v) == 2 * w.B * w.H * w.N ** 2 * (2 * e + r)
+
+
+def test_grouped_workloads_use_the_paper_head_counts():
+    g = _golden_setting()
+    pairs = {tuple(int(x) for x in p.split("/")) for p in g["gqa_heads"]}
+    found = {(w.H, w.kv_heads) for w in si.WORKLOADS.values()
+             if w.kv_heads != w.H and w.N == 8192 and w.H > 32}
+    assert pairs <= found
