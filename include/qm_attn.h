@@ -18,10 +18,12 @@
  *   - All tensor pointers are DEVICE pointers owned by the caller.  The library
  *     never allocates, frees, retains or synchronises them.
  *   - q and o are contiguous row-major [B][H][N][d] arrays, k and v
- *     [B][Hkv][N][d] (Hkv = H except in qm_attn_fwd_gqa; in qm_attn_fwd_mla
- *     v and o have their own head dimension), of the 16-bit type named by
- *     `dtype`; o has the input type.  lse is a contiguous [B][H][N] float32
- *     array.  Base pointers must be 16-byte aligned.
+ *     [B][Hkv][N][d] (Hkv = H except in qm_attn_fwd_gqa and the _layout
+ *     calls; in qm_attn_fwd_mla v and o have their own head dimension; the
+ *     _layout calls also take [B][N][heads][d]), of the 16-bit type named by
+ *     `dtype` (FP8 calls: one-byte E4M3 codes, bf16 o); otherwise o has the
+ *     input type.  lse is a contiguous [B][H][N] float32 array.  Base
+ *     pointers must be 16-byte aligned.
  *   - The call validates its arguments on the host, then enqueues one kernel on
  *     `stream` (NULL = the null stream) and returns; results are valid once the
  *     caller has synchronised that stream.  On any error nothing is enqueued and
@@ -200,7 +202,10 @@ int qm_attn_fwd_layout(const void* q, const void* k, const void* v, void* o, flo
  * query head h reads key/value head h / (H / Hkv), as in qm_attn_fwd_gqa),
  * and q, k, v and o are stored as `layout` (QM_BHND or QM_BNHD, as in
  * qm_attn_fwd_layout).  The arithmetic, its error bound and the status codes
- * are those of qm_attn_fwd_fp8.
+ * are those of qm_attn_fwd_fp8, plus QM_ERR_SHAPE for an Hkv that is below 1,
+ * above H or not a divisor of H, and QM_ERR_LAYOUT for any other layout.
+ * Hkv = H with QM_BHND is exactly qm_attn_fwd_fp8; both layouts give
+ * byte-identical results.
  */
 int qm_attn_fwd_fp8_layout(const void* q, const void* k, const void* v, void* o, float* lse,
                            int B, int H, int Hkv, int N, int d, float q_scale, float k_scale,

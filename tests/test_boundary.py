@@ -323,3 +323,22 @@ def test_product_path_does_not_import_the_oracle():
                 text = open(os.path.join(dirpath, fn)).read()
                 assert not re.search(r"^\s*(from|import)\s+oracle", text, re.M), fn
                 assert "softmax_attention" not in text, fn
+
+
+def test_c_client_builds_and_checks_buffer_sizes(lib):
+    """The plain-C client of the C ABI (driven on the GPU by
+    test_gpu_c_client.py) compiles with gcc against include/qm_attn.h, links
+    the library, and refuses a buffer smaller than its shape before any HIP
+    call."""
+    import ctypes
+    import numpy as np
+    from tests import build_c_client, test_gpu_c_client as tc
+    if not os.path.exists(build_c_client.OUT):
+        build_c_client.build()
+    client = tc.load_client()
+    x = np.zeros(16, dtype=np.uint16)
+    msg = ctypes.create_string_buffer(128)
+    st = client.qmc_run(0, x.ctypes.data, x.nbytes, x.ctypes.data, x.nbytes, x.ctypes.data,
+                        x.nbytes, x.ctypes.data, x.nbytes, x.ctypes.data, x.nbytes,
+                        1, 2, 2, 128, 64, 64, 0.125, 0, 0, 0, 1.0, 1.0, 1.0, msg, len(msg))
+    assert st == -100 and b"smaller" in msg.value
