@@ -74,6 +74,26 @@ def make_qkv(B: int, H: int, N: int, d: int, dtype: str, seed: int = 0,
     return tuple(out)
 
 
+def make_qkv_periodic_bnhd(B: int, H: int, N: int, d: int, dtype: str, period: int,
+                           seed: int = 0, Hkv: int | None = None):
+    """Large inputs at the cost of small ones: Q, K and V are drawn as
+    ``make_qkv`` draws them for ``period`` tokens and repeated along the token
+    axis up to N tokens (token t holds the draw of token t mod period).  They
+    are returned contiguous in [B][N][heads][d] order.  An odd period keeps
+    rows whose distance is a power of two distinct, so an address that wraps
+    at a power of two reads different data."""
+    q0, k0, v0 = make_qkv(B, H, period, d, dtype, seed=seed, Hkv=Hkv)
+    out = []
+    for x in (q0, k0, v0):
+        xt = np.swapaxes(x, 1, 2)                     # [B][period][heads][d]
+        y = np.empty((B, N) + xt.shape[2:], dtype=x.dtype)
+        for t in range(0, N, period):
+            n = min(period, N - t)
+            y[:, t:t + n] = xt[:, :n]
+        out.append(y)
+    return tuple(out)
+
+
 # ---------------------------------------------------------------- FP8 inputs
 # OCP E4M3FN: 1 sign, 4 exponent (bias 7) and 3 mantissa bits; no infinities;
 # S.1111.111 is NaN; the largest finite value is 448.

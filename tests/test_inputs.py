@@ -166,3 +166,12 @@ def test_grouped_workloads_use_the_paper_head_counts():
     found = {(w.H, w.kv_heads) for w in si.WORKLOADS.values()
              if w.kv_heads != w.H and w.N == 8192 and w.H > 32}
     assert pairs <= found
+
+
+def test_periodic_inputs_repeat_the_small_draw():
+    q, k, v = si.make_qkv_periodic_bnhd(2, 4, 23, 8, "bf16", period=5, seed=9, Hkv=2)
+    q0, k0, v0 = si.make_qkv(2, 4, 5, 8, "bf16", seed=9, Hkv=2)
+    assert q.shape == (2, 23, 4, 8) and k.shape == (2, 23, 2, 8) and q.flags.c_contiguous
+    for big, small in ((q, q0), (k, k0), (v, v0)):
+        for t in range(23):
+            assert np.array_equal(big[:, t], small[:, :, t % 5])
