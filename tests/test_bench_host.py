@@ -1,0 +1,65 @@
+"""The host side of bench.py, without a GPU: the one-GPU contract, the HBM
+traffic figure that follows the kernel source, and the CPU oracle legs."""
+from __future__ import annotations
+
+import os
+import re
+import shutil
+import sys
+
+import pytest
+
+import bench
+import seeded_inputs as si
+
+
+def test_more_than_one_gpu_exits_with_a_message(monkeypatch, capsys):
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--gpus", "2"])
+    with pytest.raises(SystemExit) as e:
+        bench.main()
+    assert e.value.code == 2
+    assert "one GPU" in capsys.readouterr().err
+
+
+def test_traffic_is_reported_only_for_the_profiled_kernel_source(monkeypatch, tmp_path):
+    text = open(bench.TRAFFIC_SUMMARY).read()
+    value = float(re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text).group(1))
+    assert bench.committed_traffic() == value
+    # the counter summary is for the current kernel source; any other source
+    # (here: one more comment line) gets no traffic figure
+    src = tmp_path / "kernel.hip"
+    shutil.copy(bench.KERNEL_SOURCE, src)
+    with open(src, "a") as f:
+        f.write("// edited\n")
+    monkeypatch.setattr(bench, "KERNEL_SOURCE", str(src))
+    assert bench.committed_traffic() is None
+
+
+def test_every_profile_summary_names_the_current_kernel_source():
+    """Each committed rocprofv3 summary that records a kernel source hash
+    records the current one (a kernel change needs fresh profiles)."""
+    sha = bench.kernel_source_sha256()
+    prof = os.path.join(os.path.dirname(bench.TRAFFIC_SUMMARY))
+    found = 0
+    for name in sorted(os.listdir(prof)):
+        m = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", open(os.path.join(prof, name)).read())
+        if m:
+            found += 1
+            assert m.group(1) == sha, f"{name} was measured on another kernel source"
+    assert found >= 2
+
+
+def test_cpu_baseline_reports_the_oracle_on_host_cores():
+    w = si.WORKLOADS["mha_b1_h2_n128_d64_f16"]
+    q, k, v = w.inputs()
+    r = bench.cpu_baseline(w, q, k, v, max_workers=2)
+    assert r["kind"] == "oracle" and r["unit"] == "TFLOPS"
+    assert 1 <= r["cores"] <= 2 and r["value"] > 0
+    assert "2 of 2 (batch, head) slices" in r["sample"]
+
+
+def test_cpu_single_core_times_whole_small_workloads():
+    r = bench.cpu_single_core(names=("mha_b1_h2_n128_d64_f16",))
+    assert set(r) == {"mha_b1_h2_n128_d64_f16"}
+    assert r["mha_b1_h2_n128_d64_f16"]["seconds"] >= 0
+    assert r["mha_b1_h2_n128_d64_f16"]["gflops"] > 0
