@@ -69,6 +69,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <type_traits>
 
 #include "attn_fwd_launch.h"
@@ -928,9 +929,21 @@ hipError_t launch_instance(const KParams& kp, hipStream_t stream) {
   auto kern = attn_fwd_kernel<DK, DV, DT, CAUSAL>;
   constexpr size_t lds = lds_bytes<DK, DV, DT>();
   static_assert(lds <= 160 * 1024, "one workgroup's LDS fits a CU");
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (attr != hipSuccess) return attr;
+  // The dynamic LDS limit is a per-device attribute of the kernel: raise it
+  // once on each device this instance runs on (bit d of `ready`: device d;
+  // devices past 63 set it on every call).  Concurrent first calls may both
+  // set it, which is harmless.
+  static std::atomic<uint64_t> ready{0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const uint64_t bit = dev < 64 ? 1ull << dev : 0;
+  if (!bit || !(ready.load(std::memory_order_acquire) & bit)) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    ready.fetch_or(bit, std::memory_order_release);
+  }
   hipLaunchKernelGGL(kern, dim3(kp.total), dim3(kThreads), lds, stream, kp);
   return hipGetLastError();
 }
