@@ -28,7 +28,12 @@
  *     `stream` (NULL = the null stream) and returns; results are valid once the
  *     caller has synchronised that stream.  On any error nothing is enqueued and
  *     no output is written.
- *   - Calls are thread-safe; calls on different streams may run concurrently.
+ *   - Calls are thread-safe; calls on different streams may run concurrently,
+ *     and calls may be captured into a HIP graph (nothing but the one kernel
+ *     launch is enqueued).
+ *   - Input elements are expected to be finite.  An infinite or NaN element of
+ *     q, k or v gives unspecified values in the output rows it reaches; memory
+ *     accesses and the kernel's control flow never depend on element values.
  */
 #ifndef QM_ATTN_H
 #define QM_ATTN_H
