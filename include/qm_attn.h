@@ -32,8 +32,9 @@
  *     and calls may be captured into a HIP graph (nothing but the one kernel
  *     launch is enqueued).
  *   - Input elements are expected to be finite.  An infinite or NaN element of
- *     q, k or v gives unspecified values in the output rows it reaches; memory
- *     accesses and the kernel's control flow never depend on element values.
+ *     q, k or v gives unspecified values in the output rows it reaches; the
+ *     addresses the kernel touches, its barriers and its loop trip counts never
+ *     depend on element values.
  */
 #ifndef QM_ATTN_H
 #define QM_ATTN_H
