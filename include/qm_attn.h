@@ -31,10 +31,12 @@
  *   - Calls are thread-safe; calls on different streams may run concurrently,
  *     and calls may be captured into a HIP graph (nothing but the one kernel
  *     launch is enqueued).
- *   - Input elements are expected to be finite.  An infinite or NaN element of
- *     q, k or v gives unspecified values in the output rows it reaches; the
- *     addresses the kernel touches, its barriers and its loop trip counts never
- *     depend on element values.
+ *   - Input elements are expected to be finite.  An infinite or NaN element
+ *     gives unspecified values in the outputs that read it: its own query row
+ *     (an element of q), or every row of the query heads that use its
+ *     key/value head (an element of k or v).  All other outputs are unaffected,
+ *     and the addresses the kernel touches, its barriers and its loop trip
+ *     counts never depend on element values.
  */
 #ifndef QM_ATTN_H
 #define QM_ATTN_H

@@ -294,3 +294,30 @@ def test_invalid_arguments_enqueue_nothing(qa):
     with pytest.raises(qa.QmAttnError) as e:
         qa.fwd(y, y, y, out=y)
     assert e.value.status == qa.QM_ERR_ALIAS
+
+
+def test_non_finite_inputs_stay_in_the_outputs_that_read_them(qa):
+    """NaN in one query row, and infinity in one key of one key/value head:
+    every other output matches the oracle on the same inputs, and the kernel
+    completes."""
+    import torch
+    B, H, Hkv, N, d = 2, 4, 2, 300, 128
+    q, k, v = si.make_qkv(B, H, N, d, "bf16", seed=130, Hkv=Hkv)
+    q = q.copy()
+    k = k.copy()
+    q[1, 3, 17, 5] = 0x7FC0          # bf16 NaN in query row 17 of (batch 1, head 3)
+    k[0, 1, 200, 9] = 0x7F80         # bf16 +inf in key 200 of (batch 0, kv head 1)
+    scale = si.default_scale(d)
+    clean = np.ones((B, H, N), dtype=bool)
+    clean[1, 3, 17] = False
+    clean[0, 2:4] = False            # query heads 2 and 3 read kv head 1
+    qc, kc = q.copy(), k.copy()
+    qc[1, 3, 17, 5] = 0
+    kc[0, 1, 200, 9] = 0
+    for causal in (False, True):
+        o, lse = qa.fwd(*(to_device(x, "bf16") for x in (q, k, v)), causal=causal, scale=scale)
+        torch.cuda.synchronize()
+        O, L = to_host64(o), to_host64(lse)
+        Or, lr = attention_fp64(qc, kc, v, scale, causal, "bf16")
+        check_close(O[clean], L[clean], Or[clean], lr[clean], "bf16",
+                    f"finite outputs next to non-finite inputs causal={causal}")
