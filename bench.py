@@ -50,7 +50,19 @@ PEAK_FLOP_PER_CLK = 256 * 4096  # 256 CUs x 4096 dense bf16 flop per clock
 PEAK_TFLOPS_FP8 = 5000.0
 PEAK_FLOP_PER_CLK_FP8 = 256 * 8192
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2506_12355_amd", "csrc", "attn_fwd_gfx950.hip")
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_fwd_bf16_d128_n8192_hbm_traffic.md")
+PROFILES = os.path.join(ROOT, "profiles")
+# rocprofv3 HBM-counter summaries ([B][H][N][d] layout): workload -> file; each
+# gives the HBM bytes of one launch of the workload's dominant instance (the
+# unmasked one when the workload runs both masks)
+TRAFFIC_SUMMARIES = {
+    "mha_b2_h32_n8192_d128_bf16": "attn_fwd_bf16_d128_n8192_hbm_traffic.md",
+    "fp8_b2_h32_n8192_d128": "attn_fwd_fp8_e4m3_d128_n8192_hbm_traffic.md",
+    "gqa_b2_h64_kv8_n8192_d128_bf16_causal":
+        "attn_fwd_gqa_h64_kv8_bf16_d128_n8192_causal_hbm_traffic.md",
+    "mla_b2_h128_n8192_d192_dv128_bf16_causal":
+        "attn_fwd_mla_h128_bf16_d192_dv128_n8192_causal_hbm_traffic.md",
+}
+TRAFFIC_SUMMARY = os.path.join(PROFILES, TRAFFIC_SUMMARIES["mha_b2_h32_n8192_d128_bf16"])
 
 
 def flops(B, H, N, d, causal, dv=None):
@@ -67,11 +79,14 @@ def kernel_source_sha256() -> str:
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def committed_traffic():
-    """HBM bytes per unmasked launch from the committed counter summary, if current."""
-    if not os.path.exists(TRAFFIC_SUMMARY):
+def committed_traffic(workload: str = si.BENCH_WORKLOAD):
+    """HBM bytes per launch of the workload's dominant instance from its
+    committed counter summary, if there is one for the current kernel source."""
+    name = TRAFFIC_SUMMARIES.get(workload)
+    path = os.path.join(PROFILES, name) if name else None
+    if path is None or not os.path.exists(path):
         return None
-    text = open(TRAFFIC_SUMMARY).read()
+    text = open(path).read()
     sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
     val = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
     if not sha or not val or sha.group(1) != kernel_source_sha256():
@@ -401,8 +416,7 @@ def main():
             "peak": peak,
             "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4),
-            "traffic": (committed_traffic()
-                        if w.name == si.BENCH_WORKLOAD and args.layout == "bhnd" else None),
+            "traffic": committed_traffic(w.name) if args.layout == "bhnd" else None,
         },
     }
     if not args.no_cpu_baseline:

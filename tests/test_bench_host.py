@@ -35,6 +35,19 @@ def test_traffic_is_reported_only_for_the_profiled_kernel_source(monkeypatch, tm
     assert bench.committed_traffic() is None
 
 
+def test_every_traffic_summary_gives_its_workloads_bytes():
+    """Each workload with a counter summary gets its traffic figure, at least
+    the algorithmic bytes (Q, K, V read once, O and lse written once)."""
+    for wl in bench.TRAFFIC_SUMMARIES:
+        w = si.WORKLOADS[wl]
+        es = 1 if w.dtype == "e4m3" else 2
+        alg = (w.B * w.N * (w.H * w.d + w.kv_heads * (w.d + w.d_v)) * es
+               + w.B * w.H * w.N * (2 * w.d_v + 4))
+        t = bench.committed_traffic(wl)
+        assert t is not None and 0.99 * alg <= t <= 4 * alg, (wl, t, alg)
+    assert bench.committed_traffic("mha_b1_h2_n128_d64_f16") is None
+
+
 def test_every_profile_summary_names_the_current_kernel_source():
     """Each committed rocprofv3 summary that records a kernel source hash
     records the current one (a kernel change needs fresh profiles)."""
