@@ -19,9 +19,11 @@ Prints one JSON line.  Extra objects:
                 against the dense MFMA peak of the input type (bf16/fp16 2.5, FP8 5.0 PFLOP/s); ``traffic`` is the HBM bytes
                 per launch from rocprofv3 FETCH_SIZE + WRITE_SIZE counters
                 (scaled by a plain copy of known size), read from the
-                committed profile summary (default workload only), or null
-                once the kernel source has changed since those counters were
-                taken;
+                workload's committed profile summary (the default, FP8,
+                GQA 64/8 and MLA workloads), or null without one or once the
+                kernel source has changed since those counters were taken;
+  hbm           those bytes over the same launch's duration, in GB/s, against
+                the published 8 TB/s (null with traffic);
   cpu_baseline  the fp64 CPU oracle timed on this host on a bounded sample of
                 the same workload (whole heads, both masks), in the same unit;
   cpu_single_core  the oracle on one core over the two small workloads
@@ -47,6 +49,7 @@ METRIC = "attention fwd TFLOPS (4·B·H·N²·d, ½ if causal) and % of MFMA pea
 PEAK_TFLOPS = 2500.0          # MI355X dense bf16/fp16 MFMA, published
 PEAK_FLOP_PER_CLK = 256 * 4096  # 256 CUs x 4096 dense bf16 flop per clock
 # FP8 (E4M3) MFMA: twice the 16-bit rate, 5.0 PFLOP/s dense, published
+PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E, published
 PEAK_TFLOPS_FP8 = 5000.0
 PEAK_FLOP_PER_CLK_FP8 = 256 * 8192
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2506_12355_amd", "csrc", "attn_fwd_gfx950.hip")
@@ -372,6 +375,7 @@ def main():
     value = sum(launch_flops) / (ms_per_step * 1e-3) / 1e12
     achieved = launch_flops[0] / (launch_ms[0] * 1e-3) / 1e12
     mask_name = ["causal" if c else "unmasked" for c in masks]
+    traffic = committed_traffic(w.name) if args.layout == "bhnd" else None
 
     if args.copy_calibration:
         src = torch.empty(1 << 29, dtype=torch.int16, device=dev).fill_(1)
@@ -416,8 +420,14 @@ def main():
             "peak": peak,
             "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4),
-            "traffic": committed_traffic(w.name) if args.layout == "bhnd" else None,
+            "traffic": traffic,
         },
+        # HBM bandwidth of the same launch: the committed counter bytes over this
+        # run's launch time (null without a counter summary for this source)
+        "hbm": ({"achieved": round(traffic / (launch_ms[0] * 1e-3) / 1e9, 1),
+                 "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                 "frac": round(traffic / (launch_ms[0] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)}
+                if traffic else None),
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, q, k, v, descale=scales)
