@@ -321,3 +321,24 @@ def test_non_finite_inputs_stay_in_the_outputs_that_read_them(qa):
         Or, lr = attention_fp64(qc, kc, v, scale, causal, "bf16")
         check_close(O[clean], L[clean], Or[clean], lr[clean], "bf16",
                     f"finite outputs next to non-finite inputs causal={causal}")
+
+
+def test_bench_workload_bit_stable_under_sustained_load(qa):
+    """The benchmark workload (B = 2, H = 32, N = 8192, d = 128, bf16), both
+    masks, launched back to back 40 times each as the benchmark does: every
+    launch gives the bytes of the first (the clock moves under sustained load;
+    the results must not)."""
+    import torch
+    w = si.WORKLOADS["mha_b2_h32_n8192_d128_bf16"]
+    tq, tk, tv = (to_device(x, "bf16") for x in w.inputs())
+    refs = [qa.fwd(tq, tk, tv, causal=c, scale=w.scale) for c in (False, True)]
+    torch.cuda.synchronize()
+    outs = [(torch.empty_like(o), torch.empty_like(l)) for o, l in refs]
+    mismatches = torch.zeros(2, dtype=torch.int64, device="cuda")
+    for _ in range(40):
+        for m, c in enumerate((False, True)):
+            qa.fwd(tq, tk, tv, causal=c, scale=w.scale, out=outs[m][0], lse=outs[m][1])
+            mismatches[m] += (outs[m][0].view(torch.int16) != refs[m][0].view(torch.int16)).sum()
+            mismatches[m] += (outs[m][1].view(torch.int32) != refs[m][1].view(torch.int32)).sum()
+    torch.cuda.synchronize()
+    assert mismatches.tolist() == [0, 0]
