@@ -75,8 +75,9 @@ enum {
   QM_ERR_CAUSAL = -7,      /* causal is neither 0 nor 1 */
   QM_ERR_LAUNCH = -8,      /* the HIP runtime rejected the kernel launch */
   QM_ERR_UNSUPPORTED = -9, /* a pointer is not 16-byte aligned */
-  QM_ERR_LAYOUT = -10      /* layout is not QM_BHND or QM_BNHD, or QM_BNHD with
+  QM_ERR_LAYOUT = -10,     /* layout is not QM_BHND or QM_BNHD, or QM_BNHD with
                               d_qk = 192 */
+  QM_ERR_TILE = -11        /* qm_attn_set_tile_rows: rows is not 0, 128 or 256 */
 };
 
 /*
@@ -219,6 +220,27 @@ int qm_attn_fwd_fp8_layout(const void* q, const void* k, const void* v, void* o,
                            int B, int H, int Hkv, int N, int d, float q_scale, float k_scale,
                            float v_scale, float scale, int causal, hipStream_t stream,
                            int layout);
+
+/*
+ * qm_attn_set_tile_rows - a tuning control: the query rows one workgroup
+ * owns, for every later call in the process.
+ *
+ *   rows = 0 (the default): chosen per call from the shape.  256-row
+ *            workgroups (eight wavefronts, one per CU) keep each K/V block in
+ *            LDS for the most rows; 128-row workgroups (four wavefronts, two
+ *            per CU) overlap one workgroup's start and end with the other's
+ *            work, and run when N <= 2048 or when 256-row workgroups would be
+ *            fewer than the device's CUs.
+ *   rows = 128 or 256: that size wherever it exists ([B][H][N][d] tensors with
+ *            head dimension 64 or 128; everything else runs 256).
+ *
+ * Results do not depend on it: every query row takes the same arithmetic in
+ * the same order, so outputs are byte-identical either way; only speed
+ * changes.  Returns QM_OK, or QM_ERR_TILE for any other value (the setting is
+ * then unchanged).  Thread-safe; a call racing with attention calls on other
+ * threads may or may not apply to them.
+ */
+int qm_attn_set_tile_rows(int rows);
 
 /* qm_attn_strerror - a static, human-readable string for a status code. */
 const char* qm_attn_strerror(int status);

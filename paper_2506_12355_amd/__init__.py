@@ -22,6 +22,7 @@ from .binding import (  # noqa: F401
     QM_ERR_NULL,
     QM_ERR_SCALE,
     QM_ERR_SHAPE,
+    QM_ERR_TILE,
     QM_ERR_UNSUPPORTED,
     QM_F16,
     QM_OK,
@@ -35,5 +36,6 @@ from .binding import (  # noqa: F401
     qm_attn_fwd_gqa,
     qm_attn_fwd_layout,
     qm_attn_fwd_mla,
+    set_tile_rows,
     strerror,
 )

@@ -33,6 +33,7 @@ QM_ERR_CAUSAL = -7
 QM_ERR_LAUNCH = -8
 QM_ERR_UNSUPPORTED = -9
 QM_ERR_LAYOUT = -10
+QM_ERR_TILE = -11
 
 _lib = None
 _lock = threading.Lock()
@@ -95,6 +96,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
             ctypes.c_void_p, ctypes.c_int,
         ]
         lib.qm_attn_fwd_fp8_layout.restype = ctypes.c_int
+        lib.qm_attn_set_tile_rows.argtypes = [ctypes.c_int]
+        lib.qm_attn_set_tile_rows.restype = ctypes.c_int
         lib.qm_attn_strerror.argtypes = [ctypes.c_int]
         lib.qm_attn_strerror.restype = ctypes.c_char_p
         _lib = lib
@@ -103,6 +106,15 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
 
 def strerror(status: int) -> str:
     return load_library().qm_attn_strerror(int(status)).decode()
+
+
+def set_tile_rows(rows: int) -> None:
+    """Query rows per workgroup for later calls: 0 (chosen from the shape, the
+    default), 128 or 256.  Outputs are byte-identical either way; only speed
+    changes (``qm_attn_set_tile_rows``)."""
+    status = load_library().qm_attn_set_tile_rows(int(rows))
+    if status != QM_OK:
+        raise QmAttnError(status, strerror(status))
 
 
 def qm_attn_fwd(q, k, v, o, lse, B, H, N, d, scale, causal, stream, dtype) -> int:

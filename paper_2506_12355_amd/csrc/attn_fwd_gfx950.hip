@@ -7,7 +7,9 @@
 // index): one workgroup owns BM = 256 query rows of one (batch, head); its
 // eight wavefronts (two per SIMD) own 32 rows each and walk the key/value
 // sequence in blocks of BN = 64 keys (the loop of the paper's Appendix B
-// listings).  A K/V block staged in LDS serves all 256 rows.
+// listings).  A K/V block staged in LDS serves all 256 rows.  For short
+// sequences the same kernel runs with four wavefronts (BM = 128) and
+// two-block rings, two workgroups per CU (see launch_attn_fwd).
 //
 // The two products use the 32x32x16 MFMA of CDNA4 (FP8 inputs: the 32x32x64
 // one, with ds_read_b64_tr_b8 for V^T and E4M3 packs for P^T; see Fp8 below):
@@ -94,10 +96,9 @@ typedef __attribute__((address_space(3))) i32x2 lds_i32x2;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 
-constexpr int kBM = 256;      // query rows per workgroup
 constexpr int kBN = 64;       // keys per block
-constexpr int kWaves = 8;     // 32 query rows per wavefront
-constexpr int kThreads = 64 * kWaves;
+// A workgroup has WAVES wavefronts (a template parameter, 8 or 4) of 32 query
+// rows each: BM = 32 WAVES query rows.
 // Largest probability allowed against a stale running maximum, 2^8: sums of
 // 64K such values stay far from fp32 overflow, and P fits fp16 and E4M3 (448).
 constexpr float kPmax = 256.0f;
@@ -203,7 +204,6 @@ struct Layout {
   static constexpr int KBYTES = NG * KGS;
   static constexpr int VBYTES = NG * VGS;
   static constexpr int BUF = KBYTES + VBYTES;     // one K tile + one V tile
-  static_assert(NG % kWaves == 0, "each wave issues whole load groups");
   static_assert(NG >= 8, "a transposing read's 8 key rows must fall in distinct groups");
   static_assert(BUF % 16 == 0, "buffers stay 16-byte aligned");
 };
@@ -211,8 +211,8 @@ struct Layout {
 // LDS layout of one K tile of DK columns of ES-byte elements: the first
 // min(DK, 128) columns as a Layout part, and (DK = 192) the remaining 64
 // columns as a second part right after it.  Each part keeps whole rows per
-// direct load.
-template <int DK, int ES = 2, int KSTEP = 16>
+// direct load; the WAVES wavefronts share a tile's loads evenly.
+template <int DK, int ES, int KSTEP, int WAVES>
 struct KTile {
   static constexpr int W0 = DK < 128 ? DK : 128;  // columns of part 0
   static constexpr int W1 = DK - W0;              // columns of part 1 (0 or 64)
@@ -221,29 +221,36 @@ struct KTile {
   static constexpr int NKS0 = W0 / KSTEP;         // GEMM-I k-steps in part 0
   static constexpr int OFF1 = L0::NG * L0::KGS;   // byte offset of part 1
   static constexpr int BYTES = OFF1 + (W1 ? L1::NG * L1::KGS : 0);
-  static constexpr int GPW0 = L0::NG / kWaves;    // direct loads per wave, part 0
-  static constexpr int GPW1 = W1 ? L1::NG / kWaves : 0;
+  static constexpr int GPW0 = L0::NG / WAVES;     // direct loads per wave, part 0
+  static constexpr int GPW1 = W1 ? L1::NG / WAVES : 0;
   static constexpr int GPW = GPW0 + GPW1;         // direct loads per wave per K block
   static_assert(W1 == 0 || W1 == 64, "K head dimensions 64, 128 and 192");
+  static_assert(L0::NG % WAVES == 0 && L1::NG % WAVES == 0,
+                "each wave issues whole load groups");
 };
 
-// Depth of the K and V rings: four 64-key blocks (one barrier per two blocks)
-// when four K and four V tiles fit the 160 KB of LDS, else two (one barrier
-// per block).
-template <int DK, int DV, int DT>
-using KTileOf = KTile<DK, Ops<DT>::ES, Ops<DT>::KSTEP>;
+// Depth of the K and V rings.  Eight-wave workgroups (one per CU): four
+// 64-key blocks (one barrier per two blocks) when four K and four V tiles fit
+// the 160 KB of LDS, else two (one barrier per block).  Four-wave workgroups:
+// two blocks, so that two workgroups share a CU and one's prologue and
+// epilogue overlap the other's key loop.
+template <int DK, int DV, int DT, int WAVES>
+using KTileOf = KTile<DK, Ops<DT>::ES, Ops<DT>::KSTEP, WAVES>;
 template <int DV, int DT>
 using VTileOf = Layout<DV * Ops<DT>::ES, Ops<DT>::kFp8 ? 16 : 64>;
 
-template <int DK, int DV, int DT>
+template <int DK, int DV, int DT, int WAVES>
 constexpr int ring_depth() {
-  return 4 * (KTileOf<DK, DV, DT>::BYTES + VTileOf<DV, DT>::VBYTES) <= 160 * 1024 ? 4 : 2;
+  return WAVES == 8 && 4 * (KTileOf<DK, DV, DT, WAVES>::BYTES + VTileOf<DV, DT>::VBYTES) <=
+                           160 * 1024
+             ? 4
+             : 2;
 }
 
-template <int DK, int DV, int DT>
+template <int DK, int DV, int DT, int WAVES>
 constexpr size_t lds_bytes() {
-  return (size_t)ring_depth<DK, DV, DT>() *
-         (KTileOf<DK, DV, DT>::BYTES + VTileOf<DV, DT>::VBYTES);
+  return (size_t)ring_depth<DK, DV, DT, WAVES>() *
+         (KTileOf<DK, DV, DT, WAVES>::BYTES + VTileOf<DV, DT>::VBYTES);
 }
 
 // Slot of exponential chunk c (of 16) in region 1 of NSLOT slots, and the
@@ -308,18 +315,20 @@ __device__ __forceinline__ void lds_load16(i32x4 rs, uint32_t lds, uint32_t voff
                :: "v"(voff), "{m0}"(lds), "s"(rs) : "memory");
 }
 
-template <int DK, int DV, int DT, bool CAUSAL>
-__global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
+template <int DK, int DV, int DT, bool CAUSAL, int WAVES>
+__global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attn_fwd_kernel(KParams p) {
   using OP = Ops<DT>;
   using Frag = typename OP::Frag;        // one MFMA A or B operand
   constexpr bool FP8 = OP::kFp8;
   constexpr int ES = OP::ES;             // bytes per input element
-  using KT = KTileOf<DK, DV, DT>;        // K tile (DK columns)
+  using KT = KTileOf<DK, DV, DT, WAVES>; // K tile (DK columns)
   using LV = VTileOf<DV, DT>;            // V tile (DV columns)
   constexpr int NKS = DK / OP::KSTEP;    // GEMM-I k-steps
   constexpr int NMT = DV / 32;           // GEMM-II M tiles
-  constexpr int GPWV = LV::NG / kWaves;  // V direct loads per wave per block
-  constexpr int RING = ring_depth<DK, DV, DT>();
+  constexpr int BM = 32 * WAVES;         // query rows per workgroup
+  static_assert(LV::NG % WAVES == 0, "each wave issues whole load groups");
+  constexpr int GPWV = LV::NG / WAVES;   // V direct loads per wave per block
+  constexpr int RING = ring_depth<DK, DV, DT, WAVES>();
   // Deferred GEMM-II: with four-block rings, GEMM-II of block j can run in
   // block j+1's region, interleaved with that block's exponentials and GEMM-I,
   // so that no MFMA-only stretch remains in a block.  Used where the
@@ -385,7 +394,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
   const i32x4 rv0 = i32x4{rv[0], rv[1], 0, rv[3]};
 
   auto run = [&](int qb) __attribute__((always_inline)) {
-    const int q0 = qb * kBM;
+    const int q0 = qb * BM;
     const int qw = q0 + wave * 32;   // first query row of this wavefront
     const int qrow = qw + l32;       // the query row whose column this lane holds
 
@@ -408,7 +417,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
       if (p.qmode == kQZero) qf[ks] = Frag{};
     }
 
-    const int kv_end = CAUSAL ? min(N, q0 + kBM) : N;
+    const int kv_end = CAUSAL ? min(N, q0 + BM) : N;
     const int nkv = (kv_end + kBN - 1) / kBN;
 
     f32x16 oacc[NMT];
@@ -924,11 +933,11 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(KParams p) {
   }
 }
 
-template <int DK, int DV, int DT, bool CAUSAL>
+template <int DK, int DV, int DT, bool CAUSAL, int WAVES>
 hipError_t launch_instance(const KParams& kp, hipStream_t stream) {
-  auto kern = attn_fwd_kernel<DK, DV, DT, CAUSAL>;
-  constexpr size_t lds = lds_bytes<DK, DV, DT>();
-  static_assert(lds <= 160 * 1024, "one workgroup's LDS fits a CU");
+  auto kern = attn_fwd_kernel<DK, DV, DT, CAUSAL, WAVES>;
+  constexpr size_t lds = lds_bytes<DK, DV, DT, WAVES>();
+  static_assert(lds * (8 / WAVES) <= 160 * 1024, "the workgroups of a CU fit its LDS");
   // The dynamic LDS limit is a per-device attribute of the kernel: raise it
   // once on each device this instance runs on (bit d of `ready`: device d;
   // devices past 63 set it on every call).  Concurrent first calls may both
@@ -944,13 +953,49 @@ hipError_t launch_instance(const KParams& kp, hipStream_t stream) {
     if (e != hipSuccess) return e;
     ready.fetch_or(bit, std::memory_order_release);
   }
-  hipLaunchKernelGGL(kern, dim3(kp.total), dim3(kThreads), lds, stream, kp);
+  hipLaunchKernelGGL(kern, dim3(kp.total), dim3(64 * WAVES), lds, stream, kp);
   return hipGetLastError();
+}
+
+template <int DK, int DV, int DT, int WAVES>
+hipError_t launch_masks(const KParams& kp, bool causal, hipStream_t stream) {
+  return causal ? launch_instance<DK, DV, DT, true, WAVES>(kp, stream)
+                : launch_instance<DK, DV, DT, false, WAVES>(kp, stream);
+}
+
+template <int DK, int DV, int DT>
+hipError_t launch_waves(const KParams& kp, bool causal, int waves, hipStream_t stream) {
+  return waves == 4 ? launch_masks<DK, DV, DT, 4>(kp, causal, stream)
+                    : launch_masks<DK, DV, DT, 8>(kp, causal, stream);
 }
 
 }  // namespace
 
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
+  // Workgroup size.  Eight waves (256 query rows, one workgroup per CU) keep
+  // K/V tiles in LDS for the most rows; four waves (128 rows, two-block rings,
+  // two workgroups per CU) let one workgroup's prologue and epilogue run
+  // beside the other's key loop, which wins where workgroups are short
+  // (N <= 2048) or where 256-row workgroups would leave CUs idle.  Both give
+  // the same bytes: a query row's arithmetic does not depend on its tile.
+  // The [B][N][H][d] layout and 192-wide keys run eight waves only.
+  int waves = 8;
+  if (a.layout == 0 && a.d != 192) {
+    if (a.tile_rows == 128) {
+      waves = 4;
+    } else if (a.tile_rows == 0) {
+      const long long nq8 = (a.N + 255) / 256;
+      const long long wg8 = (a.causal ? (nq8 + 1) / 2 : nq8) * a.B * a.H;
+      int dev = 0, cus = 0;
+      const bool have_cus =
+          hipGetDevice(&dev) == hipSuccess &&
+          hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+          cus > 0;
+      if (a.N <= 2048 || (have_cus && wg8 < cus)) waves = 4;
+    }
+  }
+  const int bm = 32 * waves;
+
   KParams kp;
   kp.q = static_cast<const uint8_t*>(a.q);
   kp.k = static_cast<const uint8_t*>(a.k);
@@ -961,7 +1006,7 @@ hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
   kp.H = a.H;
   kp.Hkv = a.Hkv;
   kp.group = a.H / a.Hkv;
-  kp.nq = (a.N + kBM - 1) / kBM;
+  kp.nq = (a.N + bm - 1) / bm;
   kp.wg_per_head = a.causal ? (kp.nq + 1) / 2 : kp.nq;
   kp.total = kp.wg_per_head * a.B * a.H;
   kp.c = a.c;
@@ -969,23 +1014,19 @@ hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
   kp.qmode = a.qmode;
   kp.layout = a.layout;
   // head dimensions (d_qk, d_v): 64/64, 128/128, 192/128; FP8: 128/128
-  const int dims = a.d == 64 ? 0 : (a.d == 128 ? 1 : 2);
-  const int key = a.dtype == 2 ? 12 + a.causal : dims * 4 + a.dtype * 2 + a.causal;
-  switch (key) {
-    case 0: return launch_instance<64, 64, 0, false>(kp, stream);
-    case 1: return launch_instance<64, 64, 0, true>(kp, stream);
-    case 2: return launch_instance<64, 64, 1, false>(kp, stream);
-    case 3: return launch_instance<64, 64, 1, true>(kp, stream);
-    case 4: return launch_instance<128, 128, 0, false>(kp, stream);
-    case 5: return launch_instance<128, 128, 0, true>(kp, stream);
-    case 6: return launch_instance<128, 128, 1, false>(kp, stream);
-    case 7: return launch_instance<128, 128, 1, true>(kp, stream);
-    case 8: return launch_instance<192, 128, 0, false>(kp, stream);
-    case 9: return launch_instance<192, 128, 0, true>(kp, stream);
-    case 10: return launch_instance<192, 128, 1, false>(kp, stream);
-    case 11: return launch_instance<192, 128, 1, true>(kp, stream);
-    case 12: return launch_instance<128, 128, 2, false>(kp, stream);
-    case 13: return launch_instance<128, 128, 2, true>(kp, stream);
+  const bool causal = a.causal != 0;
+  if (a.dtype == 2) return launch_waves<128, 128, 2>(kp, causal, waves, stream);
+  if (a.d == 64) {
+    return a.dtype == 0 ? launch_waves<64, 64, 0>(kp, causal, waves, stream)
+                        : launch_waves<64, 64, 1>(kp, causal, waves, stream);
+  }
+  if (a.d == 128) {
+    return a.dtype == 0 ? launch_waves<128, 128, 0>(kp, causal, waves, stream)
+                        : launch_waves<128, 128, 1>(kp, causal, waves, stream);
+  }
+  if (a.d == 192) {
+    return a.dtype == 0 ? launch_masks<192, 128, 0, 8>(kp, causal, stream)
+                        : launch_masks<192, 128, 1, 8>(kp, causal, stream);
   }
   return hipErrorInvalidValue;
 }

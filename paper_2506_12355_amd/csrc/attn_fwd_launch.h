@@ -31,9 +31,11 @@ struct AttnArgs {
   float vscale; // factor applied to O: 1, or the FP8 value scale
   int qmode;    // QMode
   int layout;   // 0: [B][heads][N][width], 1: [B][N][heads][width] (q, k, v, o)
+  int tile_rows;  // query rows per workgroup: 0 = chosen from the shape, 128 or 256
 };
 
-// Enqueues the kernel instance for (d, dv, dtype, causal).  Arguments have been
+// Enqueues the kernel instance for (d, dv, dtype, causal, workgroup size).
+// Arguments have been
 // validated by the caller.  Returns the HIP launch status.
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream);
 

@@ -4,6 +4,7 @@
 
 #include "qm_attn.h"
 
+#include <atomic>
 #include <float.h>
 #include <limits.h>
 #include <math.h>
@@ -30,6 +31,9 @@ bool finite_bits(float x) {
 
 constexpr int kFp8 = 2;   // internal dtype code: FP8 E4M3 inputs, bf16 output
 
+// query rows per workgroup: 0 = chosen per call from the shape (qm_attn_set_tile_rows)
+std::atomic<int> g_tile_rows{0};
+
 // Validation and dispatch shared by the entry points: H query heads read Hkv
 // key/value heads (Hkv == H for plain multi-head attention); q and k have head
 // dimension d, v and o head dimension dv.  dtype kFp8: q, k, v hold one-byte
@@ -52,7 +56,7 @@ int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, i
   // in 32 bits; the workgroup count fits an int
   if ((uint64_t)(N + 256) * (uint64_t)d >= (1ull << 31) || bh >= (1ull << 62) / nd)
     return QM_ERR_SHAPE;
-  if ((uint64_t)((N + 255) / 256) * bh > (uint64_t)INT_MAX) return QM_ERR_SHAPE;
+  if ((uint64_t)((N + 127) / 128) * bh > (uint64_t)INT_MAX) return QM_ERR_SHAPE;   // 128-row tiles
   if (dtype != QM_F16 && dtype != QM_BF16 && dtype != kFp8) return QM_ERR_DTYPE;
   if (!finite_bits(scale) || !finite_bits(qs) || !finite_bits(ks) || !finite_bits(vs))
     return QM_ERR_SCALE;
@@ -114,6 +118,7 @@ int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, i
     a.qmode = qk < 0.0 ? qm::kQNegate : qm::kQNormal;
   }
   a.layout = layout;
+  a.tile_rows = g_tile_rows.load(std::memory_order_relaxed);
   return qm::launch_attn_fwd(a, stream) == hipSuccess ? QM_OK : QM_ERR_LAUNCH;
 }
 
@@ -164,6 +169,12 @@ extern "C" int qm_attn_fwd_fp8_layout(const void* q, const void* k, const void* 
                   k_scale, v_scale, layout);
 }
 
+extern "C" int qm_attn_set_tile_rows(int rows) {
+  if (rows != 0 && rows != 128 && rows != 256) return QM_ERR_TILE;
+  g_tile_rows.store(rows, std::memory_order_relaxed);
+  return QM_OK;
+}
+
 extern "C" const char* qm_attn_strerror(int status) {
   switch (status) {
     case QM_OK: return "success";
@@ -180,6 +191,7 @@ extern "C" const char* qm_attn_strerror(int status) {
     case QM_ERR_UNSUPPORTED: return "tensor pointers must be 16-byte aligned";
     case QM_ERR_LAYOUT:
       return "layout must be QM_BHND (0), or QM_BNHD (1) with head dimension 64 or 128";
+    case QM_ERR_TILE: return "tile rows must be 0 (chosen per call), 128 or 256";
   }
   return "unknown status";
 }

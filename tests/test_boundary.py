@@ -38,7 +38,7 @@ def _declared_functions():
 
 def test_header_declares_entry_points():
     assert {"qm_attn_fwd", "qm_attn_fwd_gqa", "qm_attn_fwd_mla", "qm_attn_fwd_fp8",
-            "qm_attn_fwd_layout", "qm_attn_fwd_fp8_layout",
+            "qm_attn_fwd_layout", "qm_attn_fwd_fp8_layout", "qm_attn_set_tile_rows",
             "qm_attn_strerror"} <= set(_declared_functions())
 
 
@@ -277,6 +277,20 @@ def test_fp8_layout_row_bound_counts_one_byte_codes(lib):
     assert call_layout(qa.QM_BHND, **dict(big, dtype=qa.QM_BF16)) == qa.QM_ERR_UNSUPPORTED
 
 
+def test_tile_rows_control_accepts_only_its_values(lib):
+    try:
+        for rows in (1, 64, 192, 512, -128):
+            assert lib.qm_attn_set_tile_rows(rows) == qa.QM_ERR_TILE
+        for rows in (128, 256, 0):
+            assert lib.qm_attn_set_tile_rows(rows) == qa.QM_OK
+        with pytest.raises(qa.QmAttnError) as e:
+            qa.set_tile_rows(100)
+        assert e.value.status == qa.QM_ERR_TILE
+        assert "128 or 256" in qa.strerror(qa.QM_ERR_TILE)
+    finally:
+        lib.qm_attn_set_tile_rows(0)
+
+
 def test_16bit_entries_reject_the_fp8_code(lib):
     assert call(dtype=2) == qa.QM_ERR_DTYPE
     assert call_gqa(1, H=2, dtype=2) == qa.QM_ERR_DTYPE
@@ -293,7 +307,7 @@ def test_inputs_may_alias_each_other(lib):
 def test_strerror(lib):
     codes = [qa.QM_OK, qa.QM_ERR_NULL, qa.QM_ERR_SHAPE, qa.QM_ERR_HEADDIM, qa.QM_ERR_DTYPE,
              qa.QM_ERR_SCALE, qa.QM_ERR_ALIAS, qa.QM_ERR_CAUSAL, qa.QM_ERR_LAUNCH,
-             qa.QM_ERR_UNSUPPORTED]
+             qa.QM_ERR_UNSUPPORTED, qa.QM_ERR_LAYOUT, qa.QM_ERR_TILE]
     msgs = [qa.strerror(c) for c in codes]
     assert len(set(msgs)) == len(codes)
     assert qa.strerror(12345) == "unknown status"

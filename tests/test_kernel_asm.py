@@ -41,8 +41,15 @@ def _kernels(text):
     return out
 
 
+N_INSTANCES = 24   # eight waves: 16-bit (64,64), (128,128), (192,128) x dtype x mask and FP8
+                   # (128,128) x mask; four waves: the same without (192,128)
+
+
 def test_all_instances_compiled(asm):
-    assert len(_kernels(asm)) == 14   # 16-bit (64,64), (128,128), (192,128) x dtype x mask; FP8 128 x mask
+    names = list(_kernels(asm))
+    assert len(names) == N_INSTANCES
+    assert sum("ELi8EEEv" in n for n in names) == 14
+    assert sum("ELi4EEEv" in n for n in names) == 10
 
 
 def test_direct_loads_have_no_sgpr_hazard(asm):
@@ -63,7 +70,7 @@ def test_fp8_products_use_the_unscaled_mfma(asm):
     to the unscaled 32x32x64 instruction; a block-scaled form with scale code 0
     would multiply every product by 2^-254."""
     fp8 = {n: i for n, i in _kernels(asm).items() if "ELi2ELb" in n}   # dtype 2: FP8
-    assert len(fp8) == 2
+    assert len(fp8) == 4   # two masks, two workgroup sizes
     for name, insts in fp8.items():
         ops = [i.split()[0] for i in insts]
         assert ops.count("v_mfma_f32_32x32x64_f8f6f4") >= 8, name
@@ -73,8 +80,8 @@ def test_fp8_products_use_the_unscaled_mfma(asm):
 def test_no_spills_or_scratch(asm):
     spills = [int(x) for x in re.findall(r"\.vgpr_spill_count:\s+(\d+)", asm)]
     scratch = [int(x) for x in re.findall(r"\.private_segment_fixed_size:\s+(\d+)", asm)]
-    assert len(spills) == 14 and max(spills) == 0
-    assert len(scratch) == 14 and max(scratch) == 0
+    assert len(spills) == N_INSTANCES and max(spills) == 0
+    assert len(scratch) == N_INSTANCES and max(scratch) == 0
 
 
 def test_checker_sees_a_planted_hazard():
