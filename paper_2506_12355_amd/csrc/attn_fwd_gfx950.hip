@@ -315,8 +315,16 @@ __device__ __forceinline__ void lds_load16(i32x4 rs, uint32_t lds, uint32_t voff
                :: "v"(voff), "{m0}"(lds), "s"(rs) : "memory");
 }
 
+// Workgroups per CU the register budget is sized for: one of eight waves; two
+// of four waves, or three at d = 64 (168 VGPRs, 33 KB of LDS each), where the
+// third workgroup's waves fill the latency of the exponential-bound loop.
+template <int DK, int WAVES>
+constexpr int wgs_per_cu() {
+  return WAVES == 8 ? 1 : (DK == 64 ? 3 : 2);
+}
+
 template <int DK, int DV, int DT, bool CAUSAL, int WAVES>
-__global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void attn_fwd_kernel(KParams p) {
+__global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fwd_kernel(KParams p) {
   using OP = Ops<DT>;
   using Frag = typename OP::Frag;        // one MFMA A or B operand
   constexpr bool FP8 = OP::kFp8;
@@ -937,7 +945,7 @@ template <int DK, int DV, int DT, bool CAUSAL, int WAVES>
 hipError_t launch_instance(const KParams& kp, hipStream_t stream) {
   auto kern = attn_fwd_kernel<DK, DV, DT, CAUSAL, WAVES>;
   constexpr size_t lds = lds_bytes<DK, DV, DT, WAVES>();
-  static_assert(lds * (8 / WAVES) <= 160 * 1024, "the workgroups of a CU fit its LDS");
+  static_assert(lds * wgs_per_cu<DK, WAVES>() <= 160 * 1024, "the workgroups of a CU fit its LDS");
   // The dynamic LDS limit is a per-device attribute of the kernel: raise it
   // once on each device this instance runs on (bit d of `ready`: device d;
   // devices past 63 set it on every call).  Concurrent first calls may both
