@@ -94,3 +94,16 @@ def test_checker_sees_a_planted_hazard():
     assert dma_sgpr_hazards(ok) == []
     other = ["v_readlane_b32 s9, v243, 3", "buffer_load_dwordx4 v1, s[4:7], 0 offen lds"]
     assert dma_sgpr_hazards(other) == []
+
+
+def test_register_budgets_admit_the_planned_occupancy(asm):
+    """Two waves per SIMD for every instance (at most 256 VGPRs), and three
+    four-wave workgroups per CU at d = 64 (at most 168 VGPRs: three waves of
+    a SIMD's 512)."""
+    names = re.findall(r"\.name:\s+(\S*attn_fwd_kernel\S*)", asm)
+    vgprs = [int(x) for x in re.findall(r"\.vgpr_count:\s+(\d+)", asm)]
+    assert len(names) == len(vgprs) == N_INSTANCES
+    for name, v in zip(names, vgprs):
+        assert v <= 256, (name, v)
+        if "ILi64ELi64E" in name and "ELi4EEEv" in name:
+            assert v <= 168, (name, v)
