@@ -266,7 +266,7 @@ def run_grid(args, qa, torch, np):
         print(json.dumps({"metric": METRIC, "grid": True, "workload": name,
                           "B": w.B, "H": w.H, "N": w.N, "d": w.d, "dtype": w.dtype,
                           "peak_tflops": peak, "steps": args.steps, "warmup": args.warmup,
-                          "per_launch": per}),
+                          "tile_rows": args.tile_rows or "auto", "per_launch": per}),
               flush=True)
         del tq, tk, tv, o, lse
 
@@ -290,6 +290,9 @@ def main():
     ap.add_argument("--grid", action="store_true",
                     help="measure the paper's benchmark grid instead (one JSON line per shape; "
                          "bf16 at d = 64 and 128 with both masks, then FP8 at d = 128, causal)")
+    ap.add_argument("--tile-rows", type=int, default=0, choices=(0, 128, 256),
+                    help="query rows per workgroup (qm_attn_set_tile_rows): 0 chooses per call "
+                         "from the shape (default); outputs are identical either way")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -309,6 +312,7 @@ def main():
         print("bench.py needs a ROCm GPU", file=sys.stderr)
         sys.exit(1)
     qa.load_library()
+    qa.set_tile_rows(args.tile_rows)
 
     if args.grid:
         run_grid(args, qa, torch, np)
@@ -404,6 +408,7 @@ def main():
             "layout": "[B][N][H][d]" if args.layout == "bnhd" else "[B][H][N][d]",
             "flop_count": ("4·B·H·N²·d" if w.d_v == w.d else "2·B·H·N²·(d + d_v)") + ", ½ if causal",
             "masks": ["causal" if c else "none" for c in masks], "seed": w.seed,
+            "tile_rows": args.tile_rows or "auto",
         },
         "pct_of_peak": round(100.0 * value / peak, 2),
         "sclk_mhz": sclk.median(),
