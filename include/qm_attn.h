@@ -229,8 +229,9 @@ int qm_attn_fwd_fp8_layout(const void* q, const void* k, const void* v, void* o,
  *            workgroups (eight wavefronts, one per CU) keep each K/V block in
  *            LDS for the most rows; 128-row workgroups (four wavefronts, two
  *            per CU) overlap one workgroup's start and end with the other's
- *            work, and run when N <= 2048 or when 256-row workgroups would be
- *            fewer than the device's CUs.
+ *            work, and run when N <= 2048 or when the 256-row workgroups,
+ *            dealt out in rounds over the device's CUs, would keep them less
+ *            than 80% busy (fewer workgroups than CUs, or 1.5 rounds' worth).
  *   rows = 128 or 256: that size wherever it exists ([B][H][N][d] tensors with
  *            head dimension 64 or 128; everything else runs 256).
  *

@@ -982,11 +982,13 @@ hipError_t launch_waves(const KParams& kp, bool causal, int waves, hipStream_t s
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
   // Workgroup size.  Eight waves (256 query rows, one workgroup per CU) keep
   // K/V tiles in LDS for the most rows; four waves (128 rows, two-block rings,
-  // two workgroups per CU) let one workgroup's prologue and epilogue run
-  // beside the other's key loop, which wins where workgroups are short
-  // (N <= 2048) or where 256-row workgroups would leave CUs idle.  Both give
-  // the same bytes: a query row's arithmetic does not depend on its tile.
-  // The [B][N][H][d] layout and 192-wide keys run eight waves only.
+  // two or three workgroups per CU) let one workgroup's prologue and epilogue
+  // run beside another's key loop, which wins where workgroups are short
+  // (N <= 2048), and where the 256-row workgroups, dealt out in rounds over
+  // the CUs, would keep them under 80% busy (a lone four-wave workgroup in the
+  // last round uses its CU better than an idle CU does).  Both give the same bytes: a query row's arithmetic does not
+  // depend on its tile.  The [B][N][H][d] layout and 192-wide keys run eight
+  // waves only.
   int waves = 8;
   if (a.layout == 0 && a.d != 192) {
     if (a.tile_rows == 128) {
@@ -999,7 +1001,10 @@ hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
           hipGetDevice(&dev) == hipSuccess &&
           hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
           cus > 0;
-      if (a.N <= 2048 || (have_cus && wg8 < cus)) waves = 4;
+      // the 256-row grid's work as a share of its rounds over the CUs
+      const bool ragged =
+          have_cus && 5 * wg8 < 4 * ((wg8 + cus - 1) / cus) * (long long)cus;
+      if (a.N <= 2048 || ragged) waves = 4;
     }
   }
   const int bm = 32 * waves;
