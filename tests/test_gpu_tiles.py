@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 
 import seeded_inputs as si
-from oracle import attention_fp64
+from oracle import attention_fp64, attention_rows_fp64
 from tests.gpu_util import check_close, half_ulp, to_device, to_host64
 
 pytestmark = pytest.mark.gpu
@@ -91,3 +91,37 @@ def test_bench_shape_tiles_agree(qa):
     for causal in (False, True):
         _say(f"case bench shape tiles causal={causal}")
         _three_ways(qa, lambda: qa.fwd(tq, tk, tv, causal=causal, scale=w.scale))
+
+
+def _random_configs(n, seed):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        d = int(rng.choice([64, 128]))
+        H = int(rng.integers(1, 9))
+        out.append(dict(B=int(rng.integers(1, 4)), H=H,
+                        Hkv=int(rng.choice([x for x in range(1, H + 1) if H % x == 0])),
+                        N=int(rng.integers(1, 5000)), d=d,
+                        dtype=str(rng.choice(["f16", "bf16"])), causal=bool(rng.integers(2)),
+                        seed=int(rng.integers(1 << 30))))
+    return out
+
+
+@pytest.mark.parametrize("c", _random_configs(16, seed=2027), ids=lambda c: (
+    f"B{c['B']}H{c['H']}kv{c['Hkv']}N{c['N']}d{c['d']}{c['dtype']}{'c' if c['causal'] else 'u'}"))
+def test_random_shapes_tiles_agree(qa, c):
+    """Seeded random shapes up to N = 5000, across the automatic choice's
+    threshold: both tile sizes give the same bytes, and sampled rows match
+    the oracle."""
+    _say(f"case random tiles {c}")
+    q, k, v = si.make_qkv(c["B"], c["H"], c["N"], c["d"], c["dtype"], seed=c["seed"],
+                          Hkv=c["Hkv"])
+    tq, tk, tv = (to_device(x, c["dtype"]) for x in (q, k, v))
+    o, lse = _three_ways(qa, lambda: qa.fwd(tq, tk, tv, causal=c["causal"]))
+    rng = np.random.default_rng(c["seed"])
+    rows = [(int(rng.integers(c["B"])), int(rng.integers(c["H"])), int(rng.integers(c["N"])))
+            for _ in range(8)] + [(c["B"] - 1, c["H"] - 1, c["N"] - 1)]
+    O = np.array([to_host64(o[b, h, i]) for b, h, i in rows])
+    L = np.array([float(lse[b, h, i]) for b, h, i in rows])
+    Or, lr = attention_rows_fp64(q, k, v, si.default_scale(c["d"]), c["causal"], c["dtype"], rows)
+    check_close(O, L, Or, lr, c["dtype"], f"random tiles {c}")
