@@ -8,8 +8,8 @@
 // eight wavefronts (two per SIMD) own 32 rows each and walk the key/value
 // sequence in blocks of BN = 64 keys (the loop of the paper's Appendix B
 // listings).  A K/V block staged in LDS serves all 256 rows.  For short
-// sequences the same kernel runs with four wavefronts (BM = 128) and
-// two-block rings, two workgroups per CU (see launch_attn_fwd).
+// sequences the same kernel runs with four wavefronts (BM = 128) and several
+// workgroups per CU (see ring_depth, wgs_per_cu and launch_attn_fwd).
 //
 // The two products use the 32x32x16 MFMA of CDNA4 (FP8 inputs: the 32x32x64
 // one, with ds_read_b64_tr_b8 for V^T and E4M3 packs for P^T; see Fp8 below):
@@ -231,9 +231,10 @@ struct KTile {
 
 // Depth of the K and V rings.  Eight-wave workgroups (one per CU): four
 // 64-key blocks (one barrier per two blocks) when four K and four V tiles fit
-// the 160 KB of LDS, else two (one barrier per block).  Four-wave workgroups:
-// two blocks, so that two workgroups share a CU and one's prologue and
-// epilogue overlap the other's key loop.
+// the 160 KB of LDS, else two (one barrier per block).  Four-wave workgroups
+// share a CU two or three at a time, so that one's prologue and epilogue
+// overlap another's key loop: two blocks, except for FP8, whose one-byte
+// tiles fit four-block rings (and the deferred GEMM-II) twice over.
 template <int DK, int DV, int DT, int WAVES>
 using KTileOf = KTile<DK, Ops<DT>::ES, Ops<DT>::KSTEP, WAVES>;
 template <int DV, int DT>
@@ -241,8 +242,8 @@ using VTileOf = Layout<DV * Ops<DT>::ES, Ops<DT>::kFp8 ? 16 : 64>;
 
 template <int DK, int DV, int DT, int WAVES>
 constexpr int ring_depth() {
-  return WAVES == 8 && 4 * (KTileOf<DK, DV, DT, WAVES>::BYTES + VTileOf<DV, DT>::VBYTES) <=
-                           160 * 1024
+  return (WAVES == 8 || Ops<DT>::kFp8) &&
+                 4 * (KTileOf<DK, DV, DT, WAVES>::BYTES + VTileOf<DV, DT>::VBYTES) <= 160 * 1024
              ? 4
              : 2;
 }
@@ -981,14 +982,15 @@ hipError_t launch_waves(const KParams& kp, bool causal, int waves, hipStream_t s
 
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
   // Workgroup size.  Eight waves (256 query rows, one workgroup per CU) keep
-  // K/V tiles in LDS for the most rows; four waves (128 rows, two-block rings,
-  // two or three workgroups per CU) let one workgroup's prologue and epilogue
-  // run beside another's key loop, which wins where workgroups are short
-  // (N <= 2048), and where the 256-row workgroups, dealt out in rounds over
-  // the CUs, would keep them under 80% busy (a lone four-wave workgroup in the
-  // last round uses its CU better than an idle CU does).  Both give the same bytes: a query row's arithmetic does not
-  // depend on its tile.  The [B][N][H][d] layout and 192-wide keys run eight
-  // waves only.
+  // K/V tiles in LDS for the most rows; four waves (128 rows, two or three
+  // workgroups per CU) let one workgroup's prologue and epilogue run beside
+  // another's key loop.  That wins where workgroups are short (N <= 2048;
+  // FP8, whose four-wave workgroups keep four-block rings: N <= 4096), and
+  // where the 256-row workgroups, dealt out in rounds over the CUs, would
+  // keep them under 80% busy (a lone four-wave workgroup in the last round
+  // uses its CU better than an idle CU does).  Both give the same bytes: a
+  // query row's arithmetic does not depend on its tile.  The [B][N][H][d]
+  // layout and 192-wide keys run eight waves only.
   int waves = 8;
   if (a.layout == 0 && a.d != 192) {
     if (a.tile_rows == 128) {
@@ -1004,7 +1006,8 @@ hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
       // the 256-row grid's work as a share of its rounds over the CUs
       const bool ragged =
           have_cus && 5 * wg8 < 4 * ((wg8 + cus - 1) / cus) * (long long)cus;
-      if (a.N <= 2048 || ragged) waves = 4;
+      // FP8 four-wave workgroups keep four-block rings and stay ahead longer
+      if (a.N <= (a.dtype == 2 ? 4096 : 2048) || ragged) waves = 4;
     }
   }
   const int bm = 32 * waves;
