@@ -101,7 +101,7 @@ def committed_traffic(workload: str = si.BENCH_WORKLOAD):
 # shader clock during the timed region (rocm-smi, sampled from a thread)
 # --------------------------------------------------------------------------
 class SclkSampler:
-    """Samples the current SCLK with rocm-smi while the timed steps run."""
+    """Samples the current SCLK with rocm-smi from a thread while GPU work runs."""
 
     def __init__(self, period_s=0.2, enabled=True):
         import threading
@@ -143,12 +143,31 @@ class SclkSampler:
             self._thread.join(timeout=15)
 
     def median(self):
-        # fewer than three readings means the timed region was shorter than a
-        # couple of rocm-smi calls: the readings may come from idle time
+        # fewer than three readings: too few to trust (a reading may straddle
+        # the start or the end of the load)
         if len(self.samples) < 3:
             return None
         v = sorted(self.samples)
         return v[len(v) // 2]
+
+
+def sustained_sclk(step, sync, seconds=3.0, max_steps=5000, enabled=True):
+    """The shader clock under this workload: rocm-smi readings (every 0.1 s)
+    over an untimed pass that keeps running the same step for ``seconds``,
+    started right after the timed steps.  (The timed region can be far
+    shorter than one rocm-smi call.)  Returns (median MHz or None, readings,
+    steps run)."""
+    if not enabled:
+        return None, 0, 0
+    n = 0
+    with SclkSampler(period_s=0.1) as sclk:
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < seconds and n < max_steps:
+            for _ in range(8):
+                step()
+            sync()
+            n += 8
+    return sclk.median(), len(sclk.samples), n
 
 
 # --------------------------------------------------------------------------
@@ -165,9 +184,41 @@ def _oracle_head(args):
         return time.perf_counter() - t0
 
 
-def cpu_baseline(w, q, k, v, max_workers=16, descale=None):
+# CPUs one GPU's share of a shared GPU host may keep busy: worker pools never
+# exceed it, whatever the affinity mask shows
+CPU_SHARE_PER_GPU = 16
+
+
+def usable_cpus():
+    """(CPUs this process may run on, CPUs it may keep busy at once): the
+    scheduler affinity, and that count capped by the cgroup's CPU quota
+    (cgroup v2 ``cpu.max``, or v1 ``cpu.cfs_quota_us`` / ``cpu.cfs_period_us``)
+    when one is set, and by one GPU's CPU share of the host (16)."""
+    import math
+    affinity = len(os.sched_getaffinity(0))
+    quota = None
+    try:
+        with open("/sys/fs/cgroup/cpu.max") as f:
+            q, period = f.read().split()[:2]
+        if q != "max":
+            quota = int(q) / int(period)
+    except (OSError, ValueError):
+        try:
+            with open("/sys/fs/cgroup/cpu/cpu.cfs_quota_us") as f:
+                q = int(f.read())
+            with open("/sys/fs/cgroup/cpu/cpu.cfs_period_us") as f:
+                period = int(f.read())
+            if q > 0:
+                quota = q / period
+        except (OSError, ValueError):
+            pass
+    usable = affinity if quota is None else max(1, min(affinity, math.ceil(quota)))
+    return affinity, min(usable, CPU_SHARE_PER_GPU)
+
+
+def cpu_baseline(w, q, k, v, descale=None):
     import multiprocessing as mp
-    cores = max(1, min(max_workers, len(os.sched_getaffinity(0))))
+    affinity, cores = usable_cpus()
     n_heads = min(w.B * w.H, 4 * cores)
     group = w.H // w.kv_heads
     heads = [(i // w.H, i % w.H) for i in range(n_heads)]
@@ -192,9 +243,13 @@ def cpu_baseline(w, q, k, v, max_workers=16, descale=None):
         "value": round(work / wall / 1e12, 6),
         "unit": "TFLOPS",
         "cores": cores,
+        "cores_in_affinity": affinity,
         "kind": "oracle",
         "sample": (f"{len(heads)} of {w.B * w.H} (batch, head) slices of {w.name}, {masks}, "
-                   f"spread over {cores} processes with single-threaded BLAS on {model}; "
+                   f"spread over {cores} processes with single-threaded BLAS (every CPU this "
+                   f"process may keep busy: {affinity} in its affinity mask, capped by the "
+                   f"cgroup CPU quota and by one GPU's share of the host, "
+                   f"{CPU_SHARE_PER_GPU}) on {model}; "
                    f"wall {wall:.1f} s"),
     }
 
@@ -365,12 +420,13 @@ def main():
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(masks) + 1)]
               for _ in range(args.steps)]
     torch.cuda.synchronize(dev)
-    with SclkSampler(enabled=not args.no_sclk) as sclk:
-        t0 = time.perf_counter()
-        for i in range(args.steps):
-            step(events[i])
-        torch.cuda.synchronize(dev)
-        wall = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - t0
+    sclk_mhz, sclk_n, sclk_steps = sustained_sclk(step, lambda: torch.cuda.synchronize(dev),
+                                                  enabled=not args.no_sclk)
 
     launch_ms = [sum(e[m].elapsed_time(e[m + 1]) for e in events) / len(events)
                  for m in range(len(masks))]
@@ -411,9 +467,12 @@ def main():
             "tile_rows": args.tile_rows or "auto",
         },
         "pct_of_peak": round(100.0 * value / peak, 2),
-        "sclk_mhz": sclk.median(),
-        "pct_of_peak_at_sclk": (round(100.0 * value / (peak_per_clk * sclk.median() * 1e6 / 1e12), 2)
-                                if sclk.median() else None),
+        "sclk_mhz": sclk_mhz,
+        "pct_of_peak_at_sclk": (round(100.0 * value / (peak_per_clk * sclk_mhz * 1e6 / 1e12), 2)
+                                if sclk_mhz else None),
+        "sclk_source": (f"median of {sclk_n} rocm-smi readings over {sclk_steps} more steps "
+                        "of the same workload, untimed, right after the timed steps"
+                        if sclk_mhz else None),
         "per_launch": {
             name: {"ms": round(ms, 4), "tflops": round(f / (ms * 1e-3) / 1e12, 2)}
             for name, ms, f in zip(mask_name, launch_ms, launch_flops)

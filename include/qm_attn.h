@@ -37,6 +37,14 @@
  *     key/value head (an element of k or v).  All other outputs are unaffected,
  *     and the addresses the kernel touches, its barriers and its loop trip
  *     counts never depend on element values.
+ *   - Range: the kernel forms each dot product q_i . k_j in fp32 and works in
+ *     base 2, multiplying it by |scale| * log2(e) in fp32; lse is fp32 too.
+ *     Every q_i . k_j (of the stored codes, for the FP8 calls) and every
+ *     |scale * q_i . k_j| * log2(e) (FP8: with scale * q_scale * k_scale)
+ *     must therefore be finite in fp32, i.e. below 3.4e38.  A row with a
+ *     larger one gets unspecified O and lse (in practice NaN or infinity);
+ *     the other rows are unaffected.  The front end rejects a combined scale
+ *     whose fp32 value overflows (QM_ERR_SCALE); it cannot see the inputs.
  */
 #ifndef QM_ATTN_H
 #define QM_ATTN_H
@@ -229,7 +237,9 @@ int qm_attn_fwd_fp8_layout(const void* q, const void* k, const void* v, void* o,
  *            workgroups (eight wavefronts, one per CU) keep each K/V block in
  *            LDS for the most rows; 128-row workgroups (four wavefronts, two
  *            per CU) overlap one workgroup's start and end with the other's
- *            work, and run when N <= 2048 or when the 256-row workgroups,
+ *            work, and run when N <= 2048 (FP8: N <= 4096, where its
+ *            four-wavefront workgroups keep four-block K/V rings) or when
+ *            the 256-row workgroups,
  *            dealt out in rounds over the device's CUs, would keep them less
  *            than 80% busy (fewer workgroups than CUs, or 1.5 rounds' worth).
  *   rows = 128 or 256: that size wherever it exists ([B][H][N][d] tensors with

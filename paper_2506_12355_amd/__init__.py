@@ -9,6 +9,7 @@ narrower head than q and k (the MLA shape, 192/128).  ``fwd_fp8`` takes FP8
 operation and its arguments are documented in ``include/qm_attn.h``.
 """
 from .binding import (  # noqa: F401
+    DEBUG_LIB_PATH,
     LIB_PATH,
     QM_BF16,
     QM_BHND,
@@ -30,6 +31,7 @@ from .binding import (  # noqa: F401
     fwd,
     fwd_fp8,
     load_library,
+    open_library,
     qm_attn_fwd,
     qm_attn_fwd_fp8,
     qm_attn_fwd_fp8_layout,

@@ -12,6 +12,7 @@ import threading
 
 PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG_DIR, "libqm_attn.so")
+DEBUG_LIB_PATH = os.path.join(PKG_DIR, "libqm_attn_debug.so")
 
 # qm_dtype_t
 QM_F16 = 0
@@ -47,61 +48,71 @@ class QmAttnError(RuntimeError):
         self.status = status
 
 
+def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
+    """Argument and result types of every entry point of ``include/qm_attn.h``."""
+    lib.qm_attn_fwd.argtypes = [
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+        ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+    ]
+    lib.qm_attn_fwd.restype = ctypes.c_int
+    lib.qm_attn_fwd_gqa.argtypes = [
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+        ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+    ]
+    lib.qm_attn_fwd_gqa.restype = ctypes.c_int
+    lib.qm_attn_fwd_mla.argtypes = [
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+        ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+    ]
+    lib.qm_attn_fwd_mla.restype = ctypes.c_int
+    lib.qm_attn_fwd_fp8.argtypes = [
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+        ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_int,
+        ctypes.c_void_p,
+    ]
+    lib.qm_attn_fwd_fp8.restype = ctypes.c_int
+    lib.qm_attn_fwd_layout.argtypes = [
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+        ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+    ]
+    lib.qm_attn_fwd_layout.restype = ctypes.c_int
+    lib.qm_attn_fwd_fp8_layout.argtypes = [
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+        ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_int,
+        ctypes.c_void_p, ctypes.c_int,
+    ]
+    lib.qm_attn_fwd_fp8_layout.restype = ctypes.c_int
+    lib.qm_attn_set_tile_rows.argtypes = [ctypes.c_int]
+    lib.qm_attn_set_tile_rows.restype = ctypes.c_int
+    lib.qm_attn_strerror.argtypes = [ctypes.c_int]
+    lib.qm_attn_strerror.restype = ctypes.c_char_p
+    return lib
+
+
 def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     """Load (once) and return the HIP library; raise if it has not been built."""
     global _lib
     with _lock:
         if _lib is not None:
             return _lib
-        if not os.path.exists(path):
-            raise RuntimeError(
-                f"{path} is missing: the HIP attention library has not been built "
-                "(run `python -m paper_2506_12355_amd.build`)")
-        lib = ctypes.CDLL(path)
-        lib.qm_attn_fwd.argtypes = [
-            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-            ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-            ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
-        ]
-        lib.qm_attn_fwd.restype = ctypes.c_int
-        lib.qm_attn_fwd_gqa.argtypes = [
-            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-            ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-            ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
-        ]
-        lib.qm_attn_fwd_gqa.restype = ctypes.c_int
-        lib.qm_attn_fwd_mla.argtypes = [
-            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-            ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-            ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
-        ]
-        lib.qm_attn_fwd_mla.restype = ctypes.c_int
-        lib.qm_attn_fwd_fp8.argtypes = [
-            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-            ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-            ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_int,
-            ctypes.c_void_p,
-        ]
-        lib.qm_attn_fwd_fp8.restype = ctypes.c_int
-        lib.qm_attn_fwd_layout.argtypes = [
-            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-            ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-            ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
-        ]
-        lib.qm_attn_fwd_layout.restype = ctypes.c_int
-        lib.qm_attn_fwd_fp8_layout.argtypes = [
-            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-            ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-            ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_int,
-            ctypes.c_void_p, ctypes.c_int,
-        ]
-        lib.qm_attn_fwd_fp8_layout.restype = ctypes.c_int
-        lib.qm_attn_set_tile_rows.argtypes = [ctypes.c_int]
-        lib.qm_attn_set_tile_rows.restype = ctypes.c_int
-        lib.qm_attn_strerror.argtypes = [ctypes.c_int]
-        lib.qm_attn_strerror.restype = ctypes.c_char_p
-        _lib = lib
-        return lib
+        _lib = open_library(path)
+        return _lib
+
+
+def open_library(path: str) -> ctypes.CDLL:
+    """A separate handle on a build of the library at ``path`` (the tests use
+    it for the checking build, ``libqm_attn_debug.so``); raises if missing."""
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"{path} is missing: the HIP attention library has not been built "
+            "(run `python -m paper_2506_12355_amd.build`)")
+    return _declare(ctypes.CDLL(path))
 
 
 def strerror(status: int) -> str:
@@ -195,6 +206,7 @@ def fwd_fp8(q, k, v, scales, causal: bool = False, scale: float | None = None, o
         lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
     elif lse.shape != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous():
         raise ValueError("lse must be a contiguous float32 tensor of shape [B, H, N]")
+    _check_outputs_on(q.device, out, lse)
     if stream is None:
         stream = torch.cuda.current_stream(q.device)
     qs, ks, vs = (float(t) for t in scales)
@@ -220,6 +232,14 @@ def qm_attn_fwd_fp8_layout(q, k, v, o, lse, B, H, Hkv, N, d, q_scale, k_scale, v
     return load_library().qm_attn_fwd_fp8_layout(
         q, k, v, o, lse, int(B), int(H), int(Hkv), int(N), int(d), float(q_scale),
         float(k_scale), float(v_scale), float(scale), int(causal), stream, int(layout))
+
+
+def _check_outputs_on(device, out, lse) -> None:
+    """The kernel writes o and lse through device pointers: both must live on
+    the inputs' device (a host tensor's address would be written by the GPU)."""
+    for name, t in (("out", out), ("lse", lse)):
+        if not t.is_cuda or t.device != device:
+            raise ValueError(f"{name} must be on the inputs' device {device}, not {t.device}")
 
 
 def _dtype_code(t) -> int:
@@ -285,6 +305,7 @@ def fwd(q, k, v, causal: bool = False, scale: float | None = None, out=None, lse
         lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
     elif lse.shape != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous():
         raise ValueError("lse must be a contiguous float32 tensor of shape [B, H, N]")
+    _check_outputs_on(q.device, out, lse)
     if stream is None:
         stream = torch.cuda.current_stream(q.device)
     with torch.cuda.device(q.device):

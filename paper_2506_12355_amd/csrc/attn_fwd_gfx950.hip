@@ -107,6 +107,17 @@ constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data
 // s_waitcnt immediate for vmcnt(0) and lgkmcnt(0): the direct LDS loads of
 // this wave have landed
 constexpr int kWaitLoads = 0x0070;
+// Checking build (compiled with -DQM_DEBUG_SYNC): every key block ends with a
+// barrier (after this wave's loads and LDS reads have completed), on top of the
+// ring protocol's own barriers.  Extra barriers only remove overlap, so this
+// build must give the same bytes as the release build; a difference would
+// expose a read of a ring slot that its loads had not yet filled, or a load
+// into a slot that another wave was still reading.
+#ifdef QM_DEBUG_SYNC
+constexpr bool kDebugSync = true;
+#else
+constexpr bool kDebugSync = false;
+#endif
 
 struct KParams {
   const uint8_t* q;   // 16-bit or FP8 elements, addressed in bytes
@@ -836,14 +847,14 @@ __global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fw
   #pragma unroll
         for (int n = 0; n < n_dma(ph); ++n) dma(ph, n, j);
       }
-      if (RING == 2 || Q % 2 == 1) sync();
+      if (RING == 2 || Q % 2 == 1 || kDebugSync) sync();
     };
     // a block this wave skips: its loads and its barrier only
     auto skipped = [&](auto ph, int j) __attribute__((always_inline)) {
       constexpr int Q = decltype(ph)::value;
   #pragma unroll
       for (int n = 0; n < n_dma(ph); ++n) dma(ph, n, j);
-      if (RING == 2 || Q % 2 == 1) sync();
+      if (RING == 2 || Q % 2 == 1 || kDebugSync) sync();
     };
 
     load_k(0, 0);

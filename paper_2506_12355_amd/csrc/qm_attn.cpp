@@ -54,9 +54,9 @@ int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, i
   const uint64_t ndv = (uint64_t)N * (uint64_t)dv;
   // a head's byte offsets, including the padded last 256-row query block, fit
   // in 32 bits; the workgroup count fits an int
-  if ((uint64_t)(N + 256) * (uint64_t)d >= (1ull << 31) || bh >= (1ull << 62) / nd)
+  if (((uint64_t)N + 256) * (uint64_t)d >= (1ull << 31) || bh >= (1ull << 62) / nd)
     return QM_ERR_SHAPE;
-  if ((uint64_t)((N + 127) / 128) * bh > (uint64_t)INT_MAX) return QM_ERR_SHAPE;   // 128-row tiles
+  if ((((uint64_t)N + 127) / 128) * bh > (uint64_t)INT_MAX) return QM_ERR_SHAPE;   // 128-row tiles
   if (dtype != QM_F16 && dtype != QM_BF16 && dtype != kFp8) return QM_ERR_DTYPE;
   if (!finite_bits(scale) || !finite_bits(qs) || !finite_bits(ks) || !finite_bits(vs))
     return QM_ERR_SCALE;
@@ -69,7 +69,7 @@ int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, i
     // offsets, including the padded last query block, must still fit
     const uint64_t heads = (uint64_t)(H > Hkv ? H : Hkv);
     const uint64_t row = heads * (uint64_t)d * (dtype == kFp8 ? 1u : 2u);
-    if ((uint64_t)(N + 256) * row >= (1ull << 32)) return QM_ERR_SHAPE;
+    if (((uint64_t)N + 256) * row >= (1ull << 32)) return QM_ERR_SHAPE;
   }
 
   const size_t es = dtype == kFp8 ? 1 : 2;   // bytes per q, k, v element

@@ -1,12 +1,19 @@
 """Helpers for the GPU parity tests: device transfer, the parity gate, reporting.
 
-The gate (per element): |O_gpu - O_ref| <= tol + half an ulp of the storage
-type at the output's magnitude, where tol is 2e-3 for fp16 and 1e-2 for bf16;
-|lse_gpu - lse_ref| <= 1e-3.  The half ulp is the rounding of the exact value
-to the 16-bit output type, which no storing kernel can avoid (a bf16 ulp is
-already 3.1e-2 at |O| in [4, 8)).
+The gate, per output element, against the fp64 oracle value O_ref:
+  fp16: |O_gpu - O_ref| <= 2e-3, raw, everywhere.  A correctly rounded fp16
+        output meets it wherever |O| < 8 (half an fp16 ulp is at most 1.95e-3
+        there).
+  bf16: |O_gpu - O_ref| <= 1e-2, plus half a bf16 ulp of O_ref where that half
+        ulp alone exceeds 1e-2 (|O_ref| >= 4: half an ulp is 1.56e-2 in
+        [4, 8)), since no bf16-storing kernel can round such values closer.
+        The allowance is taken from the oracle's value, never from the GPU's.
+  lse:  |lse_gpu - lse_ref| <= 1e-3 (fp32 output, no storage term).
+Every comparison prints its raw max-abs O and lse errors.
 """
 from __future__ import annotations
+
+import sys
 
 import numpy as np
 
@@ -14,6 +21,11 @@ TOL = {"f16": 2e-3, "bf16": 1e-2}
 LSE_TOL = 1e-3
 _MANT = {"f16": 10, "bf16": 7}
 _EMIN = {"f16": -14, "bf16": -126}
+
+
+def say(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
 
 
 def to_device(x: np.ndarray, dtype: str):
@@ -28,6 +40,8 @@ def to_host64(t) -> np.ndarray:
 
 
 def half_ulp(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Half the spacing of the 16-bit type at |x| (the largest rounding error
+    of a round-to-nearest store of a value in x's binade)."""
     a = np.abs(np.asarray(x, dtype=np.float64))
     with np.errstate(divide="ignore"):
         e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
@@ -35,24 +49,60 @@ def half_ulp(x: np.ndarray, dtype: str) -> np.ndarray:
     return np.ldexp(0.5, (e - _MANT[dtype]).astype(np.int64))
 
 
-def check_close(O_gpu, lse_gpu, O_ref, lse_ref, dtype: str, what: str = ""):
-    """Assert the parity gate; return (raw max-abs O error, max lse error)."""
+def o_bound(O_ref: np.ndarray, dtype: str) -> np.ndarray:
+    """Per-element bound on |O_gpu - O_ref| (see the module docstring)."""
+    tol = TOL[dtype]
+    if dtype == "f16":
+        return np.full(np.shape(O_ref), tol)
+    hu = half_ulp(O_ref, dtype)
+    return tol + np.where(hu > tol, hu, 0.0)
+
+
+def compare(O_gpu, lse_gpu, O_ref, lse_ref, dtype: str, bound=None) -> dict:
+    """Gate statistics without asserting: raw max errors, count of elements
+    outside the gate and the worst one (used by :func:`check_close` and by
+    the process-parallel comparisons in ``tests/oracle_pool.py``).  ``bound``
+    replaces the 16-bit gate by a per-element bound (the FP8 tests)."""
     O_gpu = np.asarray(O_gpu, dtype=np.float64)
     lse_gpu = np.asarray(lse_gpu, dtype=np.float64)
-    assert O_gpu.shape == O_ref.shape, (O_gpu.shape, O_ref.shape)
-    assert np.all(np.isfinite(O_gpu)), f"{what}: non-finite O"
-    assert np.all(np.isfinite(lse_gpu)), f"{what}: non-finite lse"
+    if O_gpu.shape != np.shape(O_ref):
+        raise AssertionError(f"shape {O_gpu.shape} != {np.shape(O_ref)}")
+    out = {"n": int(O_gpu.size), "nonfinite_o": int(np.count_nonzero(~np.isfinite(O_gpu))),
+           "nonfinite_lse": int(np.count_nonzero(~np.isfinite(lse_gpu)))}
     err = np.abs(O_gpu - O_ref)
-    bound = TOL[dtype] + np.maximum(half_ulp(O_ref, dtype), half_ulp(O_gpu, dtype))
-    bad = err > bound
-    if np.any(bad):
-        idx = np.unravel_index(np.argmax(err - bound), err.shape)
-        raise AssertionError(
-            f"{what}: {int(bad.sum())} O elements outside the gate; worst at {idx}: "
-            f"gpu={O_gpu[idx]!r} ref={O_ref[idx]!r} err={err[idx]:.3e} bound={bound[idx]:.3e}")
+    excess = err - (o_bound(O_ref, dtype) if bound is None else bound)
+    out["max_err"] = float(err.max()) if err.size else 0.0
+    out["bad"] = int(np.count_nonzero(excess > 0))
+    if out["bad"]:
+        idx = np.unravel_index(np.argmax(excess), err.shape)
+        out["worst"] = (tuple(int(i) for i in idx), float(O_gpu[idx]), float(O_ref[idx]),
+                        float(err[idx]), float(err[idx] - excess[idx]))
     lerr = np.abs(lse_gpu - lse_ref)
-    if lerr.size and lerr.max() > LSE_TOL:
+    out["max_lse_err"] = float(lerr.max()) if lerr.size else 0.0
+    if lerr.size and out["max_lse_err"] > LSE_TOL:
         idx = np.unravel_index(np.argmax(lerr), lerr.shape)
-        raise AssertionError(f"{what}: lse err {lerr[idx]:.3e} at {idx}: "
-                             f"gpu={lse_gpu[idx]!r} ref={lse_ref[idx]!r}")
-    return float(err.max()) if err.size else 0.0, float(lerr.max()) if lerr.size else 0.0
+        out["worst_lse"] = (tuple(int(i) for i in idx), float(lse_gpu[idx]), float(lse_ref[idx]))
+    return out
+
+
+def assert_stats(st: dict, dtype: str, what: str) -> None:
+    say(f"parity {what}: {st['n']} O values ({dtype}), raw max|dO| = {st['max_err']:.3e}, "
+        f"max|dlse| = {st['max_lse_err']:.3e}")
+    assert st["nonfinite_o"] == 0, f"{what}: {st['nonfinite_o']} non-finite O values"
+    assert st["nonfinite_lse"] == 0, f"{what}: {st['nonfinite_lse']} non-finite lse values"
+    if st["bad"]:
+        idx, og, orf, e, b = st["worst"]
+        raise AssertionError(f"{what}: {st['bad']} O elements outside the gate; worst at {idx}: "
+                             f"gpu={og!r} ref={orf!r} err={e:.3e} bound={b:.3e}")
+    if st["max_lse_err"] > LSE_TOL:
+        idx, lg, lr = st["worst_lse"]
+        raise AssertionError(f"{what}: lse err {st['max_lse_err']:.3e} at {idx}: "
+                             f"gpu={lg!r} ref={lr!r}")
+
+
+def check_close(O_gpu, lse_gpu, O_ref, lse_ref, dtype: str, what: str = ""):
+    """Assert the parity gate and print the raw errors; return (raw max-abs O
+    error, max lse error)."""
+    st = compare(O_gpu, lse_gpu, O_ref, lse_ref, dtype)
+    assert_stats(st, dtype, what)
+    return st["max_err"], st["max_lse_err"]

@@ -83,6 +83,8 @@ def call(**over):
     (dict(H=-1), qa.QM_ERR_SHAPE),
     (dict(N=0), qa.QM_ERR_SHAPE),
     (dict(N=1 << 24, d=128), qa.QM_ERR_SHAPE),            # one head's slab >= 2^31 elements
+    (dict(N=(1 << 31) - 1), qa.QM_ERR_SHAPE),             # N + 256 would overflow an int
+    (dict(N=(1 << 31) - 200, d=128), qa.QM_ERR_SHAPE),
     (dict(B=1 << 30, H=1 << 30, N=1 << 16, d=64), qa.QM_ERR_SHAPE),
     (dict(d=96), qa.QM_ERR_HEADDIM),
     (dict(d=256), qa.QM_ERR_HEADDIM),
@@ -190,6 +192,7 @@ def call_layout(layout, Hkv=None, d_v=None, **over):
     (qa.QM_BNHD, dict(d=192, d_v=128), qa.QM_ERR_LAYOUT),      # 192-wide keys: [B][H][N][d] only
     # a head's rows 64 heads apart: (N + 256) * 64 * 128 * 2 bytes overflow 32 bits
     (qa.QM_BNHD, dict(N=1 << 20, H=64, d=128), qa.QM_ERR_SHAPE),
+    (qa.QM_BNHD, dict(N=(1 << 31) - 1), qa.QM_ERR_SHAPE),     # N + 256 would overflow an int
     (qa.QM_BNHD, dict(N=1 << 20, H=64, d=128, q=None), qa.QM_ERR_NULL),   # NULL comes first
     (qa.QM_BHND, dict(d=96), qa.QM_ERR_HEADDIM),
     (qa.QM_BNHD, dict(causal=3), qa.QM_ERR_CAUSAL),

@@ -51,6 +51,12 @@ def test_malformed_16bit_calls_raise(qa, qkv):
         qa.fwd(q, k, v, lse=torch.empty((1, 4, 71), dtype=torch.float32, device="cuda"))
     with pytest.raises(ValueError):
         qa.fwd(q, k.cpu(), v)                                # host tensor
+    # outputs on the host: rejected before the library is called (the kernel
+    # would write through a host address)
+    with pytest.raises(ValueError, match="out must be on"):
+        qa.fwd(q, k, v, out=torch.empty(tuple(q.shape), dtype=q.dtype))
+    with pytest.raises(ValueError, match="lse must be on"):
+        qa.fwd(q, k, v, lse=torch.empty((1, 4, 70), dtype=torch.float32))
     # value width 32 with key width 64 is no supported pair: the library says so
     with pytest.raises(qa.QmAttnError) as e:
         qa.fwd(q, k, v[:, :, :, :32].contiguous())
@@ -75,6 +81,10 @@ def test_malformed_fp8_calls_raise(qa):
     with pytest.raises(ValueError):
         qa.fwd_fp8(q8, k8, v8, s, out=torch.empty((1, 2, 40, 128), dtype=torch.float16,
                                                   device="cuda"))
+    with pytest.raises(ValueError, match="out must be on"):    # host output
+        qa.fwd_fp8(q8, k8, v8, s, out=torch.empty((1, 2, 40, 128), dtype=torch.bfloat16))
+    with pytest.raises(ValueError, match="lse must be on"):    # host lse
+        qa.fwd_fp8(q8, k8, v8, s, lse=torch.empty((1, 2, 40), dtype=torch.float32))
     with pytest.raises(qa.QmAttnError) as e:       # FP8 runs at d = 128 only
         qa.fwd_fp8(q8[..., :64].contiguous(), k8[..., :64].contiguous(),
                    v8[..., :64].contiguous(), s)

@@ -49,7 +49,10 @@ import pytest
 import seeded_inputs as si
 from oracle import (attention_fp64, attention_rows_fp64, decode_fp64, scores_fp64,
                     softmax_rows_fp64)
-from tests.gpu_util import LSE_TOL, half_ulp, to_host64
+from tests import oracle_pool
+from tests.fp8_gate import GROUP_TRUNC, rounding_bound
+from tests.fp8_gate import summation as _summation
+from tests.gpu_util import assert_stats, compare, half_ulp, to_host64
 
 pytestmark = pytest.mark.gpu
 
@@ -83,26 +86,10 @@ def _run(qa, q8, k8, v8, scales, causal, scale):
 
 
 def _gate(O, lse, Or, lr, bound, what):
-    assert O.shape == Or.shape, (O.shape, Or.shape)
-    assert np.all(np.isfinite(O)) and np.all(np.isfinite(lse)), f"{what}: non-finite output"
-    err = np.abs(O - Or)
-    bad = err > bound
-    if np.any(bad):
-        idx = np.unravel_index(np.argmax(err - bound), err.shape)
-        raise AssertionError(
-            f"{what}: {int(bad.sum())} O elements outside the gate; worst at {idx}: "
-            f"gpu={O[idx]!r} ref={Or[idx]!r} err={err[idx]:.3e} bound={bound[idx]:.3e}")
-    lerr = np.abs(lse - lr)
-    assert lerr.max() <= LSE_TOL, f"{what}: lse err {lerr.max():.3e}"
-    return float(err.max()), float(lerr.max())
-
-
-def _summation(N):
-    """Relative fp32 error allowance of the two length-N sums (O and l)."""
-    return 2 * (N + 128) * 2.0 ** -24 + 1e-5
-
-
-GROUP_TRUNC = 7 * 2.0 ** -13   # the matrix core's in-group truncation, relative
+    """Per-element bound on |O - Or|, lse within 1e-3; prints the raw errors."""
+    st = compare(O, lse, Or, lr, "bf16", bound=bound)
+    assert_stats(st, "bf16", what)
+    return st["max_err"], st["max_lse_err"]
 
 
 def _tight_case(qa, q8, k8, v8, scales, causal, scale, what, pv_trunc=False):
@@ -114,7 +101,7 @@ def _tight_case(qa, q8, k8, v8, scales, causal, scale, what, pv_trunc=False):
     PV, _ = attention_fp64(q8, k8, v8 & 0x7F, scale, causal, "e4m3", descale=scales)
     N = q8.shape[2]
     rel = _summation(N) + (GROUP_TRUNC if pv_trunc else 0.0)
-    bound = np.maximum(half_ulp(Or, "bf16"), half_ulp(O, "bf16")) + rel * PV
+    bound = half_ulp(Or, "bf16") + rel * PV
     return _gate(O, lse, Or, lr, bound, what)
 
 
@@ -181,31 +168,20 @@ def test_fp8_agrees_with_bf16_kernel(qa):
 
 # -------------------------------------------------- general FP8 inputs
 def _rounding_bound(q8, k8, v8, scales, scale, causal, rows, O, Or):
-    """The general-input bound of the module docstring, per sampled row and
-    column, from the oracle's own scores and weights."""
-    sq, sk, sv = (float(np.float32(s)) for s in scales)
-    scale64 = float(np.float32(scale))
-    cnat = abs(scale64 * sq * sk)
-    bound = np.empty_like(Or)
+    """The general-input bound (``tests/fp8_gate.py``) for the given (b, h, i)
+    rows, from the oracle's own scores and weights; O is unused (the bound
+    depends on the oracle's values only)."""
     group = q8.shape[1] // k8.shape[1]   # query heads per key/value head
-    heads = {}
+    bound = np.empty_like(Or)
+    by_head = {}
     for idx, (b, h, i) in enumerate(rows):
-        hk = h // group
-        if (b, hk) not in heads:
-            K8 = decode_fp64(k8[b, hk], "e4m3")
-            heads = {(b, hk): (K8 * sk, np.abs(K8), np.abs(decode_fp64(v8[b, hk], "e4m3")) * sv)}
-        K, Ka, Va = heads[(b, hk)]
-        Q8 = decode_fp64(q8[b, h, i:i + 1], "e4m3")
-        S = scores_fp64(Q8 * sq, K, scale64, causal, row0=i)
-        P, _ = softmax_rows_fp64(S)
-        vis = np.isfinite(S[0])
-        # largest sum of |q_c k_c| over the visible keys: the scores' truncation
-        delta = (GROUP_TRUNC + 2.0 ** -20) * cnat * float((np.abs(Q8) @ Ka[vis].T).max())
-        grow = np.exp(2 * delta)
-        pv = P[0] @ Va
-        rel = (1 + 2.0 ** -4) * grow * (1 + GROUP_TRUNC) - 1 + _summation(K.shape[0])
-        bound[idx] = rel * pv + 2.0 ** -10 * grow * P.max() * Va[vis].sum(axis=0)
-    return bound + np.maximum(half_ulp(Or, "bf16"), half_ulp(O, "bf16"))
+        by_head.setdefault((b, h), []).append((idx, i))
+    for (b, h), items in by_head.items():
+        idxs = [t for t, _ in items]
+        rr = np.array([i for _, i in items])
+        bound[idxs] = rounding_bound(q8[b, h, rr], k8[b, h // group], v8[b, h // group],
+                                     scales, scale, causal, rr, Or[idxs])
+    return bound
 
 
 def test_small_fp8_workload_full(qa):
@@ -265,6 +241,23 @@ def test_long_fp8_workload_sampled(qa, long_inputs, causal):
     _gate(O, L, Or, lr, bound, f"{w.name} causal={causal} sampled rows")
 
 
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("causal", [False, True])
+def test_long_fp8_workload_full(qa, long_inputs, causal):
+    """The FP8 benchmark workload in the launch configuration the benchmark
+    times, every output element of all 64 heads under the rounding bound (the
+    oracle spread over processes)."""
+    import torch
+    w, (q8, k8, v8, scales) = long_inputs
+    _say(f"case {w.name} causal={causal}: running (full comparison)")
+    o, lse = qa.fwd_fp8(_codes(q8), _codes(k8), _codes(v8), scales, causal=causal, scale=w.scale)
+    torch.cuda.synchronize()
+    bits, L = oracle_pool.gpu_bits(o), lse.cpu().numpy()
+    del o, lse
+    oracle_pool.full_compare(q8, k8, v8, bits, L, w.scale, causal, "e4m3",
+                             f"{w.name} causal={causal}", descale=scales)
+
+
 @pytest.mark.parametrize("name", sorted(si.GRID_FP8))
 def test_fp8_paper_grid_sampled(qa, name):
     """The paper's FP8 table configuration (16k tokens per batch, hidden 2048,
@@ -313,7 +306,7 @@ def test_fp8_outputs_written_and_nothing_else(qa):
         Or, lr = attention_fp64(q8, k8, v8, LN2, causal, "e4m3", descale=scales)
         PV, _ = attention_fp64(q8, k8, v8 & 0x7F, LN2, causal, "e4m3", descale=scales)
         O, L = to_host64(o), to_host64(lse)
-        bound = np.maximum(half_ulp(Or, "bf16"), half_ulp(O, "bf16")) + _summation(N) * PV
+        bound = half_ulp(Or, "bf16") + _summation(N) * PV
         _gate(O, L, Or, lr, bound, f"poisoned FP8 outputs causal={causal}")
 
 
@@ -339,7 +332,7 @@ def test_fp8_inputs_read_only_within_bounds(qa):
         Or, lr = attention_fp64(q8, k8, v8, LN2, causal, "e4m3", descale=scales)
         PV, _ = attention_fp64(q8, k8, v8 & 0x7F, LN2, causal, "e4m3", descale=scales)
         O, L = to_host64(o), to_host64(lse)
-        bound = np.maximum(half_ulp(Or, "bf16"), half_ulp(O, "bf16")) + _summation(N) * PV
+        bound = half_ulp(Or, "bf16") + _summation(N) * PV
         _gate(O, L, Or, lr, bound, f"guarded FP8 inputs causal={causal}")
 
 
@@ -420,7 +413,7 @@ def test_fp8_grouped_heads_and_layouts_dyadic(qa, H, Hkv, N, layout):
         O, L = to_host64(o), to_host64(lse)
         Or, lr = attention_fp64(q8, k8, v8, LN2, causal, "e4m3", descale=scales)
         PV, _ = attention_fp64(q8, k8, v8 & 0x7F, LN2, causal, "e4m3", descale=scales)
-        bound = np.maximum(half_ulp(Or, "bf16"), half_ulp(O, "bf16")) + _summation(N) * PV
+        bound = half_ulp(Or, "bf16") + _summation(N) * PV
         _gate(O, L, Or, lr, bound, what)
         _same_as_multi_head(qa, o, lse, q8, k8, v8, scales, causal, LN2)
 
@@ -461,6 +454,23 @@ def test_fp8_grouped_long_workload_sampled(qa):
     Or, lr = attention_rows_fp64(q8, k8, v8, w.scale, True, "e4m3", rows, descale=scales)
     bound = _rounding_bound(q8, k8, v8, scales, w.scale, True, rows, O, Or)
     _gate(O, L, Or, lr, bound, f"{w.name} sampled rows")
+
+
+@pytest.mark.timeout(900)
+def test_fp8_grouped_long_workload_full(qa):
+    """64 query / 8 key-value heads, N = 8192, causal: every output element of
+    all 128 query heads under the rounding bound."""
+    import torch
+    w = si.WORKLOADS["fp8_gqa_b2_h64_kv8_n8192_d128_causal"]
+    _say(f"case {w.name}: drawing inputs")
+    q8, k8, v8, scales = w.fp8_inputs()
+    _say(f"case {w.name}: running (full comparison)")
+    o, lse = qa.fwd_fp8(_codes(q8), _codes(k8), _codes(v8), scales, causal=True, scale=w.scale)
+    torch.cuda.synchronize()
+    bits, L = oracle_pool.gpu_bits(o), lse.cpu().numpy()
+    del o, lse
+    oracle_pool.full_compare(q8, k8, v8, bits, L, w.scale, True, "e4m3", w.name,
+                             descale=scales)
 
 
 @pytest.mark.parametrize("causal", [False, True])
@@ -512,5 +522,5 @@ def test_fp8_bnhd_bounds_and_outputs(qa):
         Or, lr = attention_fp64(q8, k8, v8, LN2, causal, "e4m3", descale=scales)
         PV, _ = attention_fp64(q8, k8, v8 & 0x7F, LN2, causal, "e4m3", descale=scales)
         O, L = np.swapaxes(to_host64(o), 1, 2), to_host64(lse)
-        bound = np.maximum(half_ulp(Or, "bf16"), half_ulp(O, "bf16")) + _summation(N) * PV
+        bound = half_ulp(Or, "bf16") + _summation(N) * PV
         _gate(O, L, Or, lr, bound, f"FP8 bnhd guarded causal={causal}")

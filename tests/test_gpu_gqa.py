@@ -4,7 +4,8 @@ H query heads share Hkv key/value heads; query head h reads key/value head
 h // (H / Hkv).  The oracle maps heads the same way and is otherwise the
 multi-head definition.  Small workloads are compared in full, the long ones
 (the appendix table's LLM head configurations and multi-query attention at
-N = 8192) on sampled rows.  Independently of the oracle, a grouped call must
+N = 8192) on sampled rows and then on every element, with the oracle spread
+over processes.  Independently of the oracle, a grouped call must
 equal, byte for byte, the multi-head call on K and V with every head repeated.
 """
 from __future__ import annotations
@@ -16,6 +17,7 @@ import pytest
 
 import seeded_inputs as si
 from oracle import attention_fp64, attention_rows_fp64
+from tests import oracle_pool
 from tests.gpu_util import check_close, to_device, to_host64
 
 pytestmark = pytest.mark.gpu
@@ -62,6 +64,7 @@ def _sample_rows(w, n, seed):
     return rows
 
 
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("name,causal", [
     ("gqa_b2_h64_kv8_n8192_d128_bf16_causal", True),
     ("gqa_b2_h128_kv8_n8192_d128_bf16_causal", True),
@@ -86,6 +89,11 @@ def test_long_gqa_workloads_sampled(qa, name, causal):
     Or, lr = attention_rows_fp64(q, k, v, w.scale, causal, w.dtype, rows)
     check_close(to_host64(o[ix]), to_host64(lse[ix]), Or, lr, w.dtype,
                 f"{name} causal={causal} sampled rows")
+    # then every output element, the oracle spread over processes
+    bits, L = oracle_pool.gpu_bits(o), lse.cpu().numpy()
+    del o, lse, tq, tk, tv
+    oracle_pool.full_compare(q, k, v, bits, L, w.scale, causal, w.dtype,
+                             f"{name} causal={causal}")
 
 
 @pytest.mark.parametrize("N", [1, 65, 333, 1000])

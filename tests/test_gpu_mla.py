@@ -2,8 +2,9 @@
 wide (head dimension 128 plus a 64-wide RoPE part), values and outputs 128.
 
 The oracle computes the definition with the scores over all 192 columns.
-Small workloads and edge lengths are compared in full, the DeepSeek-V3-sized
-one (128 heads, N = 8192, causal) on sampled rows.  Independently of the
+Every workload is compared in full; the long ones (including the
+DeepSeek-V3-sized one: 128 heads, N = 8192, causal) first on sampled rows,
+then on every element with the oracle spread over processes.  Independently of the
 oracle: with the last 64 query/key columns zero, the result must equal the
 128-wide multi-head kernel's byte for byte (the extra k-steps add exact zeros).
 """
@@ -16,6 +17,7 @@ import pytest
 
 import seeded_inputs as si
 from oracle import attention_fp64, attention_rows_fp64
+from tests import oracle_pool
 from tests.gpu_util import check_close, to_device, to_host64
 
 pytestmark = pytest.mark.gpu
@@ -74,6 +76,7 @@ def _sample_rows(w, n, seed):
              fixed[t] if t < len(fixed) else int(rng.integers(w.N))) for t in range(n)]
 
 
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("name,causal", [
     ("mla_b1_h16_n4096_d192_dv128_bf16", False),
     ("mla_b1_h16_n4096_d192_dv128_bf16", True),
@@ -97,6 +100,11 @@ def test_long_mla_workloads_sampled(qa, name, causal):
     Or, lr = attention_rows_fp64(q, k, v, w.scale, causal, w.dtype, rows)
     check_close(to_host64(o[ix]), to_host64(lse[ix]), Or, lr, w.dtype,
                 f"{name} causal={causal} sampled rows")
+    # then every output element, the oracle spread over processes
+    bits, L = oracle_pool.gpu_bits(o), lse.cpu().numpy()
+    del o, lse, tq, tk, tv
+    oracle_pool.full_compare(q, k, v, bits, L, w.scale, causal, w.dtype,
+                             f"{name} causal={causal}")
 
 
 @pytest.mark.parametrize("N", [200, 1000])

@@ -2,10 +2,11 @@
 
 Every case draws seeded inputs, runs ``qm_attn_fwd`` on the GPU and compares
 element by element with the oracle on the same 16-bit inputs (gate in
-``tests/gpu_util.py``).  The small workloads are compared in full; the long
-ones (N = 8192, 32768) on sampled rows that the oracle computes one by one, in
-the same launch configuration that ``bench.py`` times, plus properties that
-hold at any size.
+``tests/gpu_util.py``; every case prints its raw max-abs errors).  Every
+quoted workload is compared in full, the long ones (N = 2048, 8192, 32768) in
+the launch configuration that ``bench.py`` times, with the oracle spread over
+processes; sampled rows that the oracle computes one by one, and properties
+that hold at any size, are cheap extra checks.
 """
 from __future__ import annotations
 
@@ -59,21 +60,41 @@ def test_small_workloads_full(qa, name):
         full_case(qa, q, k, v, w.dtype, w.scale, causal, f"{name} causal={causal}")
 
 
-def test_causal_n2048_d128_f16(qa):
-    w = si.WORKLOADS["mha_b4_h32_n2048_d128_f16_causal"]
-    q, k, v = w.inputs()
-    _say(f"case {w.name}")
-    Og, lg = run_gpu(qa, q, k, v, w.dtype, w.scale, True)
-    # four heads in full (every query block), then sampled rows of all heads
-    for b, h in [(0, 0), (1, 7), (2, 19), (3, 31)]:
-        Or, lr = attention_fp64(q[b:b + 1, h:h + 1], k[b:b + 1, h:h + 1],
-                                v[b:b + 1, h:h + 1], w.scale, True, w.dtype)
-        check_close(Og[b:b + 1, h:h + 1], lg[b:b + 1, h:h + 1], Or, lr, w.dtype,
-                    f"{w.name} head ({b},{h})")
-    rows = _sample_rows(w, 96, seed=1)
-    Or, lr = attention_rows_fp64(q, k, v, w.scale, True, w.dtype, rows)
-    ix = tuple(np.array(rows).T)
-    check_close(Og[ix], lg[ix], Or, lr, w.dtype, f"{w.name} sampled rows")
+_INPUTS = {}
+
+
+def _inputs(name):
+    """Seeded inputs of a named workload, drawn once per module."""
+    if name not in _INPUTS:
+        _say(f"drawing the inputs of {name}")
+        _INPUTS.clear()
+        _INPUTS[name] = si.WORKLOADS[name].inputs()
+    return _INPUTS[name]
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name,causal", [
+    ("mha_b4_h32_n2048_d128_f16_causal", True),
+    ("mha_b2_h32_n8192_d128_bf16", False),
+    ("mha_b2_h32_n8192_d128_bf16", True),
+    ("mha_b1_h32_n32768_d128_bf16_causal_qk2", True),
+])
+def test_workloads_every_element(qa, name, causal):
+    """The quoted long workloads in the launch configuration the benchmark
+    times, every output element compared with the oracle (all heads, the
+    oracle spread over processes; ``tests/oracle_pool.py``)."""
+    import torch
+    from tests import oracle_pool
+    w = si.WORKLOADS[name]
+    q, k, v = _inputs(name)
+    tq, tk, tv = (to_device(x, w.dtype) for x in (q, k, v))
+    _say(f"case {name} causal={causal}: running (full comparison)")
+    o, lse = qa.fwd(tq, tk, tv, causal=causal, scale=w.scale)
+    torch.cuda.synchronize()
+    bits, L = oracle_pool.gpu_bits(o), lse.cpu().numpy()
+    del o, lse, tq, tk, tv
+    oracle_pool.full_compare(q, k, v, bits, L, w.scale, causal, w.dtype,
+                             f"{name} causal={causal}")
 
 
 def _sample_rows(w, n, seed):
@@ -96,8 +117,7 @@ def _sample_rows(w, n, seed):
 def test_long_workloads_sampled(qa, name, causal):
     import torch
     w = si.WORKLOADS[name]
-    _say(f"case {name} causal={causal}: drawing inputs")
-    q, k, v = w.inputs()
+    q, k, v = _inputs(name)
     tq, tk, tv = (to_device(x, w.dtype) for x in (q, k, v))
     _say(f"case {name} causal={causal}: running")
     o, lse = qa.fwd(tq, tk, tv, causal=causal, scale=w.scale)
