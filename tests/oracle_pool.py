@@ -67,10 +67,10 @@ def _head(bh):
 
 def _merge(parts):
     out = {"n": 0, "nonfinite_o": 0, "nonfinite_lse": 0, "max_err": 0.0, "bad": 0,
-           "max_lse_err": 0.0}
+           "over_tol": 0, "max_lse_err": 0.0}
     worst_excess = None
     for st in parts:
-        for key in ("n", "nonfinite_o", "nonfinite_lse", "bad"):
+        for key in ("n", "nonfinite_o", "nonfinite_lse", "bad", "over_tol"):
             out[key] += st[key]
         out["max_err"] = max(out["max_err"], st["max_err"])
         if "worst" in st:
