@@ -101,33 +101,51 @@ def committed_traffic(workload: str = si.BENCH_WORKLOAD):
 # shader clock during the timed region (rocm-smi, sampled from a thread)
 # --------------------------------------------------------------------------
 class SclkSampler:
-    """Samples the current SCLK with rocm-smi from a thread while GPU work runs."""
+    """Samples the current SCLK (and the package power, where rocm-smi reports
+    it) with rocm-smi from a thread while GPU work runs."""
 
     def __init__(self, period_s=0.2, enabled=True):
         import threading
         self.enabled = enabled
         self.period_s = period_s
         self.samples = []
+        self.power = []
         self._stop = threading.Event()
         self._thread = threading.Thread(target=self._run, daemon=True)
 
+    @staticmethod
+    def parse(text):
+        """(SCLK MHz or None, package power W or None) from rocm-smi's JSON."""
+        data = json.loads(text)
+        sclk = watts = None
+        for card in data.values():
+            if not isinstance(card, dict):
+                continue
+            m = re.search(r"(\d+)\s*Mhz", str(card.get("sclk clock speed:", "")), re.I)
+            if m and sclk is None:
+                sclk = int(m.group(1))
+            for key, val in card.items():
+                if watts is None and re.search(r"power", key, re.I) and "(W)" in key:
+                    try:
+                        watts = float(str(val).split()[0])
+                    except ValueError:
+                        pass
+        return sclk, watts
+
     def _read(self):
         import subprocess
-        out = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True,
-                             text=True, timeout=10).stdout
-        data = json.loads(out)
-        for card in data.values():
-            m = re.search(r"(\d+)\s*Mhz", str(card.get("sclk clock speed:", "")))
-            if m:
-                return int(m.group(1))
-        return None
+        out = subprocess.run(["rocm-smi", "--showclocks", "--showpower", "--json"],
+                             capture_output=True, text=True, timeout=10).stdout
+        return self.parse(out)
 
     def _run(self):
         while not self._stop.is_set():
             try:
-                v = self._read()
+                v, w = self._read()
                 if v:
                     self.samples.append(v)
+                if w:
+                    self.power.append(w)
             except Exception:
                 pass
             self._stop.wait(self.period_s)
@@ -156,9 +174,9 @@ def sustained_sclk(step, sync, seconds=3.0, max_steps=5000, enabled=True):
     over an untimed pass that keeps running the same step for ``seconds``,
     started right after the timed steps.  (The timed region can be far
     shorter than one rocm-smi call.)  Returns (median MHz or None, readings,
-    steps run)."""
+    steps run, median package power in W or None)."""
     if not enabled:
-        return None, 0, 0
+        return None, 0, 0, None
     n = 0
     with SclkSampler(period_s=0.1) as sclk:
         t0 = time.perf_counter()
@@ -167,7 +185,8 @@ def sustained_sclk(step, sync, seconds=3.0, max_steps=5000, enabled=True):
                 step()
             sync()
             n += 8
-    return sclk.median(), len(sclk.samples), n
+    watts = sorted(sclk.power)[len(sclk.power) // 2] if len(sclk.power) >= 3 else None
+    return sclk.median(), len(sclk.samples), n, watts
 
 
 # --------------------------------------------------------------------------
@@ -425,8 +444,8 @@ def main():
         step(events[i])
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - t0
-    sclk_mhz, sclk_n, sclk_steps = sustained_sclk(step, lambda: torch.cuda.synchronize(dev),
-                                                  enabled=not args.no_sclk)
+    sclk_mhz, sclk_n, sclk_steps, watts = sustained_sclk(
+        step, lambda: torch.cuda.synchronize(dev), enabled=not args.no_sclk)
 
     launch_ms = [sum(e[m].elapsed_time(e[m + 1]) for e in events) / len(events)
                  for m in range(len(masks))]
@@ -470,6 +489,7 @@ def main():
         "sclk_mhz": sclk_mhz,
         "pct_of_peak_at_sclk": (round(100.0 * value / (peak_per_clk * sclk_mhz * 1e6 / 1e12), 2)
                                 if sclk_mhz else None),
+        "package_power_w": watts,
         "sclk_source": (f"median of {sclk_n} rocm-smi readings over {sclk_steps} more steps "
                         "of the same workload, untimed, right after the timed steps"
                         if sclk_mhz else None),

@@ -47,8 +47,11 @@
 // p = 2^(c s - m) are formed against the running maximum m without first
 // reducing the block's own maximum.  A lane whose 32 probabilities sum to at
 // most 2^8 has every p <= 2^8; only when some lane exceeds that (the running
-// maximum must rise; always on the first block) is the block's exact maximum
-// taken, O and l rescaled by 2^(m_old - m_new) and the probabilities redone.
+// maximum must rise; always on the first block), or, for 16-bit inputs, when
+// the block outweighs four times the row's sum so far (its new keys dominate
+// the row, and their largest weight must be exactly 1 before it is rounded to
+// 16 bits), is the block's exact maximum taken, O and l rescaled by
+// 2^(m_old - m_new) and the probabilities redone.
 // O = sum p v / sum p and lse = (m + log2 l) ln 2 use the same m, so the
 // result is exact in either case.
 //
@@ -102,6 +105,14 @@ constexpr int kBN = 64;       // keys per block
 // Largest probability allowed against a stale running maximum, 2^8: sums of
 // 64K such values stay far from fp32 overflow, and P fits fp16 and E4M3 (448).
 constexpr float kPmax = 256.0f;
+// 16-bit inputs also take the exact path when a block's probabilities outweigh
+// kDominant times everything the row has summed before (its new keys carry
+// more than 80% of the row's weight): the new maximum is then taken exactly,
+// so the row's dominant weight is 2^0 = 1 exactly instead of a value up to 2^8
+// that rounding to bf16 for the second product can move by 2^-8 of itself
+// (an error O carries in full when that key dominates).  Rare for diffuse
+// rows; on near-one-hot rows it keeps O within 1e-2 plus half a bf16 ulp.
+constexpr float kDominant = 4.0f;
 constexpr int kXcds = 8;
 constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data
 // s_waitcnt immediate for vmcnt(0) and lgkmcnt(0): the direct LDS loads of
@@ -622,9 +633,10 @@ __global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fw
     // whose 32 probabilities sum to at most 2^8 (kPmax) has every p <= 2^8, which
     // keeps all sums in range.  Only when some lane exceeds that (the running
     // maximum must rise, and always on a wave's first block, where m_run is
-    // -inf) is the block's exact maximum taken, O and l rescaled and the
-    // probabilities recomputed.  Results are exact either way: O and lse use
-    // the same m_run.
+    // -inf), or, for 16-bit inputs, when some lane's block sum exceeds
+    // kDominant times its running sum, is the block's exact maximum taken, O
+    // and l rescaled and the probabilities recomputed.  Results are exact
+    // either way: O and lse use the same m_run.
     // vb: the V slot GEMM-II reads (block j's, or block j-1's when deferred);
     // pin: P^T of block j-1 (deferred GEMM-II); pout: P^T of block j; first:
     // block 0, which has no deferred GEMM-II to run
@@ -782,7 +794,7 @@ __global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fw
       lsum = lsum_even + lsum_odd;
 
       // exact path (rare): the running maximum rises
-      if (__any(lsum > kPmax)) {
+      if (__any(lsum > kPmax || (!FP8 && lsum > kDominant * l_run))) {
         // a use of GEMM-I's results on this path too keeps the compiler from
         // sinking GEMM-I's MFMAs out of region 1 to past this branch
         asm volatile("" :: "v"(s_next[0]), "v"(s_next[1]));

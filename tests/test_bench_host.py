@@ -97,3 +97,13 @@ def test_cpu_single_core_times_whole_small_workloads():
     assert set(r) == {"mha_b1_h2_n128_d64_f16"}
     assert r["mha_b1_h2_n128_d64_f16"]["seconds"] >= 0
     assert r["mha_b1_h2_n128_d64_f16"]["gflops"] > 0
+
+
+def test_rocm_smi_json_gives_clock_and_power():
+    """The sampler reads SCLK and a package-power key (rocm-smi JSON)."""
+    import json
+    text = json.dumps({"card0": {"sclk clock speed:": "(1804Mhz)",
+                                 "Current Socket Graphics Package Power (W)": "1397.0"},
+                       "system": {"Driver version": "6.x"}})
+    assert bench.SclkSampler.parse(text) == (1804, 1397.0)
+    assert bench.SclkSampler.parse(json.dumps({"card0": {}})) == (None, None)
