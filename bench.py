@@ -19,8 +19,8 @@ Prints one JSON line.  Extra objects:
                 against the dense MFMA peak of the input type (bf16/fp16 2.5, FP8 5.0 PFLOP/s); ``traffic`` is the HBM bytes
                 per launch from rocprofv3 FETCH_SIZE + WRITE_SIZE counters
                 (scaled by a plain copy of known size), read from the
-                workload's committed profile summary (the default, FP8,
-                GQA 64/8 and MLA workloads), or null without one or once the
+                workload's committed profile summary (every quoted 16-bit
+                workload, FP8, GQA 64/8 and MLA), or null without one or once the
                 kernel source has changed since those counters were taken;
   hbm           those bytes over the same launch's duration, in GB/s, against
                 the published 8 TB/s (null with traffic);
@@ -64,6 +64,9 @@ TRAFFIC_SUMMARIES = {
         "attn_fwd_gqa_h64_kv8_bf16_d128_n8192_causal_hbm_traffic.md",
     "mla_b2_h128_n8192_d192_dv128_bf16_causal":
         "attn_fwd_mla_h128_bf16_d192_dv128_n8192_causal_hbm_traffic.md",
+    "mha_b8_h16_n1024_d64_f16": "attn_fwd_f16_d64_n1024_b8_h16_hbm_traffic.md",
+    "mha_b4_h32_n2048_d128_f16_causal": "attn_fwd_f16_d128_n2048_b4_h32_causal_hbm_traffic.md",
+    "mha_b1_h32_n32768_d128_bf16_causal_qk2": "attn_fwd_bf16_d128_n32768_causal_qk2_hbm_traffic.md",
 }
 TRAFFIC_SUMMARY = os.path.join(PROFILES, TRAFFIC_SUMMARIES["mha_b2_h32_n8192_d128_bf16"])
 
@@ -169,12 +172,13 @@ class SclkSampler:
         return v[len(v) // 2]
 
 
-def sustained_sclk(step, sync, seconds=3.0, max_steps=5000, enabled=True):
+def sustained_sclk(step, sync, seconds=3.0, max_steps=1_000_000, enabled=True):
     """The shader clock under this workload: rocm-smi readings (every 0.1 s)
     over an untimed pass that keeps running the same step for ``seconds``,
     started right after the timed steps.  (The timed region can be far
     shorter than one rocm-smi call.)  Returns (median MHz or None, readings,
-    steps run, median package power in W or None)."""
+    steps run, median package power in W or None: not every host's rocm-smi
+    reports one)."""
     if not enabled:
         return None, 0, 0, None
     n = 0
