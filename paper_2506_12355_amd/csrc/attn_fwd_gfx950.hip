@@ -4,8 +4,9 @@
 //
 // Work decomposition (the paper's Method section gives each thread block a
 // fixed batch and head of Q, a (BM, HeadDim) tile at coordinate L = block
-// index): one workgroup owns BM = 256 query rows of one (batch, head); its
-// eight wavefronts (two per SIMD) own 32 rows each and walk the key/value
+// index): a tile is BM = 256 query rows of one (batch, head); the eight
+// wavefronts of the workgroup that owns it (two per SIMD) own 32 rows each and
+// walk the key/value
 // sequence in blocks of BN = 64 keys (the loop of the paper's Appendix B
 // listings).  A K/V block staged in LDS serves all 256 rows.  For short
 // sequences the same kernel runs with four wavefronts (BM = 128) and several
@@ -61,9 +62,13 @@
 // sequence tail.  A workgroup runs a long and a short query block, the long
 // one first, so that all workgroups cost the same.
 //
-// Dispatch order: workgroup i runs on XCD i % 8.  The linear id is remapped so
-// that consecutive query blocks of the same head (and the heads sharing one
-// key/value head) land on the same XCD and share its L2 for the K/V stream.
+// Dispatch order: workgroup i runs on XCD i % 8.  The linear tile id is
+// remapped so that consecutive query blocks of the same head (and the heads
+// sharing one key/value head) land on the same XCD and share its L2 for the
+// K/V stream.  With 16-bit inputs the workgroups are persistent: as many as
+// the CUs hold at once (a multiple of 8), workgroup w taking tiles w,
+// w + grid, ..., which keeps tile t on XCD t % 8 and the same tiles side by
+// side as one workgroup per tile would.
 //
 // Shapes: head dimension 64 or 128 (q, k, v alike), or 192-wide queries and
 // keys with 128-wide values (the MLA shape); H query heads may share Hkv
@@ -338,6 +343,15 @@ __device__ __forceinline__ void lds_load16(i32x4 rs, uint32_t lds, uint32_t voff
                :: "v"(voff), "{m0}"(lds), "s"(rs) : "memory");
 }
 
+// The lane's index in its wavefront, as volatile inline assembly so that the
+// compiler recomputes it where it is asked for instead of keeping one value
+// live (or spilled) across long stretches of code.
+__device__ __forceinline__ int lane_id() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
 // Workgroups per CU the register budget is sized for: one of eight waves; two
 // of four waves, or three at d = 64 (168 VGPRs, 33 KB of LDS each), where the
 // third workgroup's waves fill the latency of the exponential-bound loop.
@@ -372,18 +386,20 @@ __global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fw
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   char* const lds = reinterpret_cast<char*>(smem);
 
-  const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int l32 = lane & 31;
-  const int hi = lane >> 5;
   const int N = p.N;
 
-  // ---- which (batch*head) and query block(s) this workgroup owns ----
-  // Unmasked: one query block.  Causal: query block qb costs qb + 1 units of
-  // key blocks, so a workgroup takes the pair (nq-1-i, i), the longer first:
-  // every pair costs the same and the grid has no long tail.
-  int id = blockIdx.x;
+  // ---- which tiles this workgroup owns ----
+  // A tile is one (batch*head, query block), or, causal, the pair (nq-1-i, i)
+  // of query blocks (query block qb costs qb + 1 units of key blocks, so every
+  // pair costs the same and the grid has no long tail; the longer runs first).
+  // 16-bit inputs: the grid holds as many workgroups as the CUs run at once
+  // (a multiple of 8), and workgroup w walks tiles w, w + grid, ..., so the
+  // launch gap and set-up of a new workgroup are paid once per CU, not per
+  // tile.  FP8 launches one workgroup per tile (its loop measured slower).
   const int per_xcd = p.total / kXcds;
+  auto do_tile = [&](int tile) __attribute__((always_inline)) {
+  int id = tile;
   if (id < per_xcd * kXcds) id = (id % kXcds) * per_xcd + id / kXcds;
   const int bh = id / p.wg_per_head;
   const int slot_in_head = id - bh * p.wg_per_head;
@@ -425,6 +441,11 @@ __global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fw
   const i32x4 rv0 = i32x4{rv[0], rv[1], 0, rv[3]};
 
   auto run = [&](int qb) __attribute__((always_inline)) {
+    // this lane's index, formed afresh in each run: no lane value stays live
+    // from one query block to the next (kept live, it spills)
+    const int lane = lane_id();
+    const int l32 = lane & 31;
+    const int hi = lane >> 5;
     const int q0 = qb * BM;
     const int qw = q0 + wave * 32;   // first query row of this wavefront
     const int qrow = qw + l32;       // the query row whose column this lane holds
@@ -963,6 +984,17 @@ __global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fw
     if (DEFER) __syncthreads();
     run(qbs[1]);
   }
+  };
+  if constexpr (FP8) {
+    do_tile(blockIdx.x);
+  } else {
+    for (int tile = blockIdx.x; tile < p.total; tile += gridDim.x) {
+      do_tile(tile);
+      // the next tile's first loads refill ring slots that the last blocks
+      // (and a deferred GEMM-II) read
+      __syncthreads();
+    }
+  }
 }
 
 template <int DK, int DV, int DT, bool CAUSAL, int WAVES>
@@ -985,7 +1017,18 @@ hipError_t launch_instance(const KParams& kp, hipStream_t stream) {
     if (e != hipSuccess) return e;
     ready.fetch_or(bit, std::memory_order_release);
   }
-  hipLaunchKernelGGL(kern, dim3(kp.total), dim3(64 * WAVES), lds, stream, kp);
+  // 16-bit inputs: persistent workgroups, as many as the CUs hold at once,
+  // rounded down to a multiple of the XCD count so that tile t still runs on
+  // XCD t % 8 (the dispatcher deals workgroup w to XCD w % 8)
+  int grid = kp.total;
+  if (!Ops<DT>::kFp8) {
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    const int resident = cus * wgs_per_cu<DK, WAVES>() / kXcds * kXcds;
+    if (resident >= kXcds && resident < grid) grid = resident;
+  }
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * WAVES), lds, stream, kp);
   return hipGetLastError();
 }
 
