@@ -334,12 +334,14 @@ __device__ __forceinline__ i32x4 make_dma_rsrc(const void* base, uint32_t bytes)
 // direct load it waits for every load in flight before the first V read,
 // which stalls the wave mid-block.  Here the only waits are the explicit
 // ones before each barrier.  The compiler does not resolve hazards on an
-// inline instruction's operands, so the instruction carries its own five
-// wait states: a VALU write of an SGPR (for example a spill reload of the
-// descriptor) needs five before a vector memory instruction reads it, and
-// the M0 write needs one.
+// inline instruction's operands.  The one wait state the M0 write needs
+// before the load is the s_nop here.  A VALU write of an SGPR the load reads
+// (a spill reload of the descriptor with v_readlane, say) would need five;
+// the compiled kernels have none within five wait states of any direct load
+// on any path into it, which the build's assembly is checked for.  Five
+// wait states on every load instead cost 1-2.5% of the kernel's throughput.
 __device__ __forceinline__ void lds_load16(i32x4 rs, uint32_t lds, uint32_t voff) {
-  asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %0, %2, 0 offen lds"
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %2, 0 offen lds"
                :: "v"(voff), "{m0}"(lds), "s"(rs) : "memory");
 }
 
@@ -814,8 +816,12 @@ __global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fw
       __builtin_amdgcn_s_setprio(0);
       lsum = lsum_even + lsum_odd;
 
-      // exact path (rare): the running maximum rises
-      if (__any(lsum > kPmax || (!FP8 && lsum > kDominant * l_run))) {
+      // exact path (rare): the running maximum rises.  One compare against
+      // min(kPmax, kDominant * l_run), whose operands are ready before the
+      // region ends (two compares joined before the vote cost a select and a
+      // second compare on the critical path)
+      const float l_thr = FP8 ? kPmax : fminf(kPmax, kDominant * l_run);
+      if (__any(lsum > l_thr)) {
         // a use of GEMM-I's results on this path too keeps the compiler from
         // sinking GEMM-I's MFMAs out of region 1 to past this branch
         asm volatile("" :: "v"(s_next[0]), "v"(s_next[1]));
