@@ -477,7 +477,10 @@ __global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fw
     f32x16 oacc[NMT];
   #pragma unroll
     for (int mt = 0; mt < NMT; ++mt) oacc[mt] = f32x16{};
-    float m_run = -INFINITY;   // running maximum, exp2 domain
+    // running maximum, exp2 domain; -FLT_MAX (not -inf) while a lane has seen
+    // no visible key, so that it serves as the exponentials' offset directly:
+    // every visible key then overflows to +inf and forces the exact path
+    float m_run = -FLT_MAX;
     float l_run = 0.f;         // this lane's share of the running row sum
 
     // ---- HBM -> LDS: this wave's load groups of one K or V block ----
@@ -656,7 +659,7 @@ __global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fw
     // whose 32 probabilities sum to at most 2^8 (kPmax) has every p <= 2^8, which
     // keeps all sums in range.  Only when some lane exceeds that (the running
     // maximum must rise, and always on a wave's first block, where m_run is
-    // -inf), or, for 16-bit inputs, when some lane's block sum exceeds
+    // -FLT_MAX), or, for 16-bit inputs, when some lane's block sum exceeds
     // kDominant times its running sum, is the block's exact maximum taken, O
     // and l rescaled and the probabilities recomputed.  Results are exact
     // either way: O and lse use the same m_run.
@@ -697,9 +700,7 @@ __global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fw
           }
         }
       }
-      // before the first block m_run is -inf: offset by -FLT_MAX instead, so
-      // every visible key overflows to +inf and forces the exact path below
-      float mu = (m_run == -INFINITY) ? -FLT_MAX : m_run;
+      float mu = m_run;
 
       // P^T operands of GEMM-II: 16-bit, four fragments of 8 values (key step
       // u = 16 keys); FP8, one fragment of all 32 of the lane's values, byte
@@ -827,12 +828,14 @@ __global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fw
         asm volatile("" :: "v"(s_next[0]), "v"(s_next[1]));
         const float m_blk = row_max(s) * p.c;
         const float m_new = fmaxf(m_run, m_blk);
-        const float alpha = (m_run == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+        // 0 on a lane's first visible keys (m_run = -FLT_MAX); O and l are
+        // then 0 anyway
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
   #pragma unroll
         for (int mt = 0; mt < NMT; ++mt) oacc[mt] *= alpha;
         l_run *= alpha;
         m_run = m_new;
-        mu = (m_run == -INFINITY) ? 0.f : m_run;
+        mu = m_run;
         lsum = 0.f;
   #pragma unroll
         for (int i = 0; i < 16; ++i) exp_chunk(i);
