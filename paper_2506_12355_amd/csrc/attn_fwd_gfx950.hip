@@ -879,11 +879,16 @@ __global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fw
     // last row; none for a wave past the sequence end).  It still issues the
     // loads of the blocks after those, and takes every barrier.
     const int j_act = (qw >= N) ? 0 : (CAUSAL ? min(nkv, (qw + 31) / kBN + 1) : nkv);
+    // The computed blocks run in one loop and the skipped ones in a second,
+    // so that no block tests whether it computes; only the four-wave causal
+    // d = 64 instance, at its register ceiling, keeps that test inside one
+    // loop over all blocks (the split loops spill there).
+    constexpr bool kSplitLoops = DEFER || !(DK == 64 && WAVES == 4 && CAUSAL);
     auto iteration = [&](auto ph, auto first, int j, f32x16 (&s_cur)[2], f32x16 (&s_next)[2],
                          Frag (&pin)[NPB], Frag (&pout)[NPB]) __attribute__((always_inline)) {
       constexpr int Q = decltype(ph)::value;
       constexpr int VB = DEFER ? (Q + 3) % 4 : Q % RING;   // the V slot GEMM-II reads
-      if (DEFER || j < j_act) {
+      if (kSplitLoops || j < j_act) {
         block(ph, first, j, (Q + 1) % RING, VB, s_cur, s_next, pin, pout);
       } else {
   #pragma unroll
@@ -917,8 +922,9 @@ __global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fw
     using First = std::true_type;
     // Deferred: block 0 (no GEMM-II of its own to run), then the other
     // computed blocks, the skipped ones after the last GEMM-II below.
-    // Otherwise one loop over all blocks.
-    const int j_loop = DEFER ? j_act : nkv;
+    // Otherwise one loop over the computed blocks (over all blocks where
+    // kSplitLoops is off), the skipped ones after it.
+    const int j_loop = kSplitLoops ? j_act : nkv;
     if constexpr (DEFER) {
       if (j_act > 0) {
         iteration(C0{}, First{}, 0, sa, sb, p_odd, p_even);
@@ -933,13 +939,13 @@ __global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fw
         }
       }
     } else {
-      for (int j = 0; j < nkv; j += 4) {
+      for (int j = 0; j < j_loop; j += 4) {
         iteration(C0{}, Later{}, j, sa, sb, p_odd, p_even);
-        if (j + 1 >= nkv) break;
+        if (j + 1 >= j_loop) break;
         iteration(C1{}, Later{}, j + 1, sb, sa, p_even, p_odd);
-        if (j + 2 >= nkv) break;
+        if (j + 2 >= j_loop) break;
         iteration(C2{}, Later{}, j + 2, sa, sb, p_odd, p_even);
-        if (j + 3 >= nkv) break;
+        if (j + 3 >= j_loop) break;
         iteration(C3{}, Later{}, j + 3, sb, sa, p_even, p_odd);
       }
     }
