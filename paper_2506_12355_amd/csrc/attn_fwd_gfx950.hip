@@ -323,6 +323,17 @@ __device__ __forceinline__ i32x4 make_dma_rsrc(const void* base, uint32_t bytes)
                (int32_t)bytes, kRsrcWord3};
 }
 
+// The same buffer seen from byte off on (base + off, size reduced by off), or,
+// when live is false, a zero-size descriptor (a load through it touches no
+// memory and writes zeros).  A load at per-lane offset v through it reads what
+// a load at v + off through rs reads, under the same range check.  off must
+// not exceed rs's size when live.
+__device__ __forceinline__ i32x4 dma_rsrc_at(i32x4 rs, uint32_t off, bool live) {
+  const uint64_t base = ((uint64_t)(uint32_t)rs[1] << 32 | (uint32_t)rs[0]) + off;
+  return i32x4{(int32_t)(uint32_t)base, (int32_t)(uint32_t)(base >> 32),
+               live ? (int32_t)((uint32_t)rs[2] - off) : 0, rs[3]};
+}
+
 // One 16-byte-per-lane direct load HBM -> LDS: lane l's 16 bytes at byte
 // offset voff of the buffer land at LDS address lds + 16 l (M0 holds lds).
 // The whole offset is in the VGPR operand: the range check covers only that
@@ -334,15 +345,24 @@ __device__ __forceinline__ i32x4 make_dma_rsrc(const void* base, uint32_t bytes)
 // direct load it waits for every load in flight before the first V read,
 // which stalls the wave mid-block.  Here the only waits are the explicit
 // ones before each barrier.  The compiler does not resolve hazards on an
-// inline instruction's operands.  The one wait state the M0 write needs
-// before the load is the s_nop here.  A VALU write of an SGPR the load reads
-// (a spill reload of the descriptor with v_readlane, say) would need five;
-// the compiled kernels have none within five wait states of any direct load
-// on any path into it, which the build's assembly is checked for.  Five
-// wait states on every load instead cost 1-2.5% of the kernel's throughput.
+// inline instruction's operands.  WAIT wait states precede the load: one
+// (what the M0 write needs) for the loads of the key loop, where the compiled
+// kernels have no VALU write of an SGPR the load reads within five wait
+// states on any path into it (the build's assembly is checked for that);
+// five for a run's first loads, where the compiler reloads spilled
+// descriptor words with v_readlane (a VALU write of an SGPR needs five
+// before a vector memory instruction reads it).  Five on every load instead
+// cost 1-2.5% of the kernel's throughput.
+template <int WAIT>
 __device__ __forceinline__ void lds_load16(i32x4 rs, uint32_t lds, uint32_t voff) {
-  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %2, 0 offen lds"
-               :: "v"(voff), "{m0}"(lds), "s"(rs) : "memory");
+  static_assert(WAIT == 1 || WAIT == 5, "one or five wait states");
+  if constexpr (WAIT == 1) {
+    asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %2, 0 offen lds"
+                 :: "v"(voff), "{m0}"(lds), "s"(rs) : "memory");
+  } else {
+    asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %0, %2, 0 offen lds"
+                 :: "v"(voff), "{m0}"(lds), "s"(rs) : "memory");
+  }
 }
 
 // The lane's index in its wavefront, as volatile inline assembly so that the
@@ -438,9 +458,6 @@ __global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fw
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + head_off(b, h_q, p.H, WQ), span(rs_q, WQ));
   const i32x4 rk = make_dma_rsrc(p.k + head_off(b, h_kv, p.Hkv, WQ), span(rs_k, WQ));
   const i32x4 rv = make_dma_rsrc(p.v + head_off(b, h_kv, p.Hkv, WV), span(rs_v, WV));
-  // zero-size descriptors: a load through one touches no memory and writes zeros
-  const i32x4 rk0 = i32x4{rk[0], rk[1], 0, rk[3]};
-  const i32x4 rv0 = i32x4{rv[0], rv[1], 0, rv[3]};
 
   auto run = [&](int qb) __attribute__((always_inline)) {
     // this lane's index, formed afresh in each run: no lane value stays live
@@ -494,31 +511,41 @@ __global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fw
                            (uint32_t)(KT::W0 * ES + (lane % KT::L1::U) * 16);
     const uint32_t voff = (uint32_t)(LV::NG * (lane / LV::U)) * rs_v + (uint32_t)((lane % LV::U) * 16);
     auto lds_addr = [&](int byte_off) { return (uint32_t)(uintptr_t)(lds_void*)(lds + byte_off); };
+    // wait states before a direct load: a run's first loads, or the key loop's
+    using Wait5 = std::integral_constant<int, 5>;
+    using Wait1 = std::integral_constant<int, 1>;
+    // The block's first row goes into the descriptor (scalar work, once per
+    // block and tensor); the group's row and the lane's part stay in a
+    // per-lane offset that does not change from block to block.  live: the
+    // block is one this query block uses; its first row is then inside the
+    // sequence, so the shifted size does not wrap.
     // load i (of KT::GPW) of this wave for K block blk into K slot kb
-    auto k_load = [&](int i, int blk, int kb, i32x4 rs) __attribute__((always_inline)) {
+    auto k_load = [&](auto wait, int i, int blk, int kb, bool live) __attribute__((always_inline)) {
+      constexpr int W = decltype(wait)::value;
+      const i32x4 rs = dma_rsrc_at(rk, (uint32_t)(blk * kBN) * rs_k, live);
       if (i < KT::GPW0) {
         const int g = wave * KT::GPW0 + i;
-        lds_load16(rs, lds_addr(kb * KT::BYTES + g * KT::L0::KGS),
-                   koff0 + (uint32_t)(blk * kBN + g) * rs_k);
+        lds_load16<W>(rs, lds_addr(kb * KT::BYTES + g * KT::L0::KGS), koff0 + (uint32_t)g * rs_k);
       } else {
         const int g = wave * KT::GPW1 + (i - KT::GPW0);
-        lds_load16(rs, lds_addr(kb * KT::BYTES + KT::OFF1 + g * KT::L1::KGS),
-                   koff1 + (uint32_t)(blk * kBN + g) * rs_k);
+        lds_load16<W>(rs, lds_addr(kb * KT::BYTES + KT::OFF1 + g * KT::L1::KGS),
+                   koff1 + (uint32_t)g * rs_k);
       }
     };
     // load i (of GPWV) of this wave for V block blk into V slot vb
-    auto v_load = [&](int i, int blk, int vb, i32x4 rs) __attribute__((always_inline)) {
+    auto v_load = [&](auto wait, int i, int blk, int vb, bool live) __attribute__((always_inline)) {
+      constexpr int W = decltype(wait)::value;
+      const i32x4 rs = dma_rsrc_at(rv, (uint32_t)(blk * kBN) * rs_v, live);
       const int g = wave * GPWV + i;
-      lds_load16(rs, lds_addr(VOFF + vb * LV::VBYTES + g * LV::VGS),
-                 voff + (uint32_t)(blk * kBN + g) * rs_v);
+      lds_load16<W>(rs, lds_addr(VOFF + vb * LV::VBYTES + g * LV::VGS), voff + (uint32_t)g * rs_v);
     };
     auto load_k = [&](int blk, int kb) {
   #pragma unroll
-      for (int i = 0; i < KT::GPW; ++i) k_load(i, blk, kb, rk);
+      for (int i = 0; i < KT::GPW; ++i) k_load(Wait5{}, i, blk, kb, true);
     };
     auto load_v = [&](int blk, int vb) {
   #pragma unroll
-      for (int i = 0; i < GPWV; ++i) v_load(i, blk, vb, rv);
+      for (int i = 0; i < GPWV; ++i) v_load(Wait5{}, i, blk, vb, true);
     };
 
     // Direct loads issued during block j, Q = j % 4 (loads of blocks past the
@@ -538,16 +565,16 @@ __global__ __launch_bounds__(64 * WAVES, (wgs_per_cu<DK, WAVES>())) void attn_fw
       if (RING == 4 && Q % 2 == 0) {
         const int second = n >= KT::GPW ? 1 : 0;
         const int blk = j + 3 + second;
-        k_load(n - second * KT::GPW, blk, (Q + 3 + second) % 4, blk < nkv ? rk : rk0);
+        k_load(Wait1{}, n - second * KT::GPW, blk, (Q + 3 + second) % 4, blk < nkv);
       } else if (RING == 4) {
         const int second = n >= GPWV ? 1 : 0;
         const int lead = DEFER ? 0 : 1;   // deferred GEMM-II reads V(j) a block later
         const int blk = j + lead + second;
-        v_load(n - second * GPWV, blk, (Q + lead + second) % 4, blk < nkv ? rv : rv0);
+        v_load(Wait1{}, n - second * GPWV, blk, (Q + lead + second) % 4, blk < nkv);
       } else if (n < KT::GPW) {
-        k_load(n, j + 2, Q % 2, j + 2 < nkv ? rk : rk0);
+        k_load(Wait1{}, n, j + 2, Q % 2, j + 2 < nkv);
       } else {
-        v_load(n - KT::GPW, j + 1, (Q + 1) % 2, j + 1 < nkv ? rv : rv0);
+        v_load(Wait1{}, n - KT::GPW, j + 1, (Q + 1) % 2, j + 1 < nkv);
       }
     };
 
