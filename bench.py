@@ -28,6 +28,12 @@ Prints one JSON line.  Extra objects:
                 the same workload (whole heads, both masks), in the same unit;
   cpu_single_core  the oracle on one core over the two small workloads
                 (B=1 H=2 N=128 d=64 and B=8 H=16 N=1024 d=64, fp16, unmasked).
+
+``--sustain SECONDS`` replaces the timed steps by each launch run back to back
+for that long while rocm-smi samples the shader clock, one JSON line per
+launch; with ``--library PATH`` (another build of the library) two builds can
+be compared one after the other on one machine, which is the fair comparison
+on a power-limited part.
 """
 from __future__ import annotations
 
@@ -350,6 +356,43 @@ def run_grid(args, qa, torch, np):
 
 
 # --------------------------------------------------------------------------
+def sustain(args, w, masks, step_one, dev, stream, torch, peak_per_clk):
+    """Each launch of the workload back to back for args.sustain seconds (after
+    its own warm-up) while rocm-smi samples the shader clock: the throughput a
+    launch holds at the clock it settles to.  The part is power-limited with
+    random operands, so two builds of the kernel compare fairly only like this,
+    one after the other on one machine."""
+    for m, causal in enumerate(masks):
+        for _ in range(20):
+            step_one(m)
+        torch.cuda.synchronize(dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        n = 0
+        with SclkSampler(period_s=0.1) as sclk:
+            e0.record(stream)
+            t0 = time.perf_counter()
+            while time.perf_counter() - t0 < args.sustain:
+                for _ in range(16):
+                    step_one(m)
+                n += 16
+                torch.cuda.synchronize(dev)
+            e1.record(stream)
+            torch.cuda.synchronize(dev)
+        ms = e0.elapsed_time(e1) / n
+        tflops = flops(w.B, w.H, w.N, w.d, causal, w.d_v) / (ms * 1e-3) / 1e12
+        mhz = sclk.median()
+        print(json.dumps({
+            "sustained": True, "workload": w.name, "launch": "causal" if causal else "unmasked",
+            "library": os.path.abspath(args.library) if args.library else "in-tree",
+            "seconds": args.sustain, "launches": n, "ms": round(ms, 4), "tflops": round(tflops, 2),
+            "sclk_mhz": mhz,
+            "tflops_per_ghz": round(tflops / (mhz / 1000.0), 1) if mhz else None,
+            "pct_of_peak_at_sclk": (round(100.0 * tflops / (peak_per_clk * mhz * 1e6 / 1e12), 2)
+                                    if mhz else None),
+        }), flush=True)
+        time.sleep(1.0)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -373,6 +416,13 @@ def main():
                          "from the shape (default); outputs are identical either way")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM counter calibration)")
+    ap.add_argument("--sustain", type=float, default=0.0, metavar="SECONDS",
+                    help="instead of the timed steps, run each launch of the workload back to "
+                         "back for SECONDS while rocm-smi samples the shader clock, and print "
+                         "one JSON line per launch (throughput, clock, throughput per GHz)")
+    ap.add_argument("--library", default=None, metavar="PATH",
+                    help="load this build of libqm_attn.so instead of the in-tree one "
+                         "(to compare builds on one machine)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -389,7 +439,10 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a ROCm GPU", file=sys.stderr)
         sys.exit(1)
-    qa.load_library()
+    if args.library:
+        qa.load_library(os.path.abspath(args.library))
+    else:
+        qa.load_library()
     qa.set_tile_rows(args.tile_rows)
 
     if args.grid:
@@ -423,22 +476,31 @@ def main():
             for _ in masks]
     stream = torch.cuda.current_stream(dev)
 
+    def launch(m):
+        causal = masks[m]
+        if fp8:
+            qa.fwd_fp8(tq, tk, tv, scales, causal=causal, scale=w.scale, out=outs[m][0],
+                       lse=outs[m][1], stream=stream, layout=args.layout)
+        else:
+            qa.fwd(tq, tk, tv, causal=causal, scale=w.scale, out=outs[m][0],
+                   lse=outs[m][1], stream=stream, layout=args.layout)
+
     def step(ev=None):
-        for m, causal in enumerate(masks):
+        for m in range(len(masks)):
             if ev is not None:
                 ev[m].record(stream)
-            if fp8:
-                qa.fwd_fp8(tq, tk, tv, scales, causal=causal, scale=w.scale, out=outs[m][0],
-                           lse=outs[m][1], stream=stream, layout=args.layout)
-            else:
-                qa.fwd(tq, tk, tv, causal=causal, scale=w.scale, out=outs[m][0],
-                       lse=outs[m][1], stream=stream, layout=args.layout)
+            launch(m)
         if ev is not None:
             ev[len(masks)].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize(dev)
+
+    if args.sustain > 0:
+        sustain(args, w, masks, step_one=lambda m: launch(m), dev=dev, stream=stream, torch=torch,
+                peak_per_clk=peak_per_clk)
+        return
 
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(masks) + 1)]
               for _ in range(args.steps)]
@@ -458,7 +520,8 @@ def main():
     value = sum(launch_flops) / (ms_per_step * 1e-3) / 1e12
     achieved = launch_flops[0] / (launch_ms[0] * 1e-3) / 1e12
     mask_name = ["causal" if c else "unmasked" for c in masks]
-    traffic = committed_traffic(w.name) if args.layout == "bhnd" else None
+    # the committed counters belong to the in-tree kernel source
+    traffic = committed_traffic(w.name) if args.layout == "bhnd" and not args.library else None
 
     if args.copy_calibration:
         src = torch.empty(1 << 29, dtype=torch.int16, device=dev).fill_(1)
